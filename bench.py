@@ -1,0 +1,199 @@
+"""Throughput of the per-head spectral-norm path on one MI355X.
+
+One step = one spectral_step call: all layers, all query heads, n_iter
+power-iteration steps each (one W_K sweep from v, then per step one fused W_Q
+sweep and one fused W_K sweep), plus the per-layer E4M3 scale.  Weights,
+start vectors and outputs are resident in HBM before the timed region.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload KEY]
+
+Prints one JSON line.  ``value`` is heads*iterations per second over all
+layers; ``roofline`` reports the W_Q sweep kernel (the dominant one) against
+the HBM peak; ``cpu_baseline`` times the float64 oracle on host cores over a
+bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E, vendor figure
+METRIC = "heads·iters/sec (all layers) and achieved HBM GB/s vs MI355X peak"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "q_sweep_traffic.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2602_18851_amd", "csrc", "spectral.hip")
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="llama2-70b-gqa")
+    p.add_argument("--n-iter", type=int, default=0, help="override the workload's iteration count")
+    p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle CPU baseline")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    return p.parse_args()
+
+
+def source_hash() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(n_layers_bytes: float):
+    """HBM bytes per W_Q-sweep launch from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel source; else None."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha256_16") != source_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, budget_s: float, n_iter: int):
+    """The float64 oracle (per head, the paper's step order) on host cores,
+    over as many heads of the workload as fit in the time budget."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle.power_iteration import head_slices, power_iteration
+    from workloads import layer_weights, start_vectors
+
+    v0 = start_vectors(wl.replace(n_layers=1), "cpu")[0].double().numpy()
+    wq, wk = layer_weights(wl, 0, "cpu")
+    wq, wk = wq.float().numpy(), wk.float().numpy()
+    heads = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < budget_s and heads < 10 * wl.n_q:
+        h = heads % wl.n_q
+        WQ, WK = head_slices(wq, wk, h, wl.n_kv, wl.head_dim)
+        power_iteration(WQ, WK, v0[h], n_iter)
+        heads += 1
+    dt = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {
+        "value": heads * n_iter / dt,
+        "unit": "heads·iters/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"{heads} query heads of layer 0, {n_iter} iterations each, float64 numpy "
+                  f"(implicit 4-GEMV chain per head), {dt:.1f} s",
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
+        sys.exit(2)
+
+    import torch
+
+    from paper_2602_18851_amd import Spectral
+    from workloads import WORKLOADS, all_weights, start_vectors
+
+    wl = WORKLOADS[args.workload]
+    n_iter = args.n_iter or wl.n_iter
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    wq, wk = all_weights(wl, dev)
+    v0 = start_vectors(wl, dev)
+    v = v0.clone()
+    sigma = torch.empty(wl.n_layers, wl.n_q, dtype=torch.float32, device=dev)
+    scale = torch.empty(wl.n_layers, dtype=torch.float32, device=dev)
+    iters = torch.empty(wl.n_layers, wl.n_q, dtype=torch.int32, device=dev)
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=0.0)
+    torch.cuda.synchronize()
+
+    def step():
+        est.step(wq, wk, v, n_iter, sigma=sigma, scale=scale, iters=iters)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall_s = time.perf_counter() - t_wall
+    ms = e0.elapsed_time(e1) / args.steps
+    assert bool(torch.isfinite(sigma).all()) and bool((iters == n_iter).all())
+
+    # per-kernel durations, HIP events on the launch stream (separate pass)
+    est.profile(True)
+    step()
+    prof = est.profile_read()
+    est.profile(False)
+    q_ms, q_n = prof["q_sweep"]
+    k_ms, k_n = prof["k_sweep"]
+    i_ms, _ = prof["k_sweep_first"]
+    f_ms, _ = prof["finalize"]
+
+    e = wl.elem_bytes
+    H = wl.n_layers * wl.n_q
+    q_bytes, k_bytes = wl.weight_bytes()
+    q_alg = q_bytes + H * 2 * wl.head_dim * 4          # weights + z in + y out, per launch
+    q_avg_ms = q_ms / q_n
+    achieved = q_alg / (q_avg_ms * 1e-3) / 1e9
+    call_bytes = n_iter * (q_bytes + k_bytes) + k_bytes + 12 * wl.d_model * H
+    heads_iters = H * n_iter
+    out = {
+        "metric": METRIC,
+        "value": heads_iters / (ms * 1e-3),
+        "unit": "heads·iters/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.key,
+            "description": wl.description,
+            "n_layers": wl.n_layers, "d_model": wl.d_model, "n_q_heads": wl.n_q, "n_kv_heads": wl.n_kv,
+            "head_dim": wl.head_dim, "weights_dtype": wl.dtype, "n_iter": n_iter, "heads": H,
+            "start": "cold (seeded unit vectors), state carried across steps",
+        },
+        "effective_GBps": call_bytes / (ms * 1e-3) / 1e9,
+        "effective_frac_of_peak": call_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "call_bytes": call_bytes,
+        "wall_s_timed": wall_s,
+        "kernels_ms_per_step": {"k_sweep_first": i_ms, "q_sweep": q_ms, "k_sweep": k_ms, "finalize": f_ms},
+        "roofline": {
+            "kernel": "q_sweep (fused W_Q sweep)",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": measured_traffic(q_alg),
+            "algorithmic_bytes_per_launch": q_alg,
+            "avg_launch_ms": q_avg_ms,
+            "launches": q_n,
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, n_iter)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,145 @@
+/*
+ * spectral.h -- C ABI of the per-head spectral-norm estimator and the
+ * per-layer FP8 E4M3 scale factor for MI355X (gfx950).
+ *
+ * What it computes (arXiv 2602.18851):
+ *   For every layer l and query head h, sigma_h estimates
+ *   ||W^Q_h W^{K T}_{g(h)}||_2 by implicit power iteration (Sec. 4.1 and
+ *   App. E, "Power Iteration for Spectral Norm Estimation"): with one
+ *   persistent vector v per head,
+ *       z = W^{K T} v,  u' = W^Q z,  sigma = ||u'||,  u = u'/sigma,
+ *       y = W^{Q T} u,  v' = W^K y,  v = v'/||v'||,
+ *   never forming the d x d product.  Grouped-query attention uses the
+ *   unexpanded key weights (Sec. 4.2, Prop. "Implicit GQA power iteration"):
+ *   query head h reads key head g(h) = floor(h / g), g = n_q / n_kv, and each
+ *   key head's weights are read once per sweep for its whole group.
+ *   The per-layer scale is Eq. "scale" (Sec. 3.4):
+ *       scale_l = alpha * max_h sigma_h * (d / sqrt(d_h)) / (eta_fp8 * r_max).
+ *
+ * Weight layout (per layer, PyTorch Linear): wq is [n_q*d_h rows][ld],
+ * wk is [n_kv*d_h rows][ld], row-major, only the first d_model columns of a
+ * row are read.  Rows of head h are h*d_h .. h*d_h+d_h-1, i.e. the transpose
+ * of the paper's W^Q_h in R^{d x d_h}.
+ *
+ * Memory and ownership: every pointer passed to spectral_step is device
+ * memory owned by the caller and must stay valid until the work queued on the
+ * context's stream has finished.  The library owns only the context and its
+ * workspace (allocated in spectral_init, freed in spectral_destroy).
+ *
+ * Errors: functions return SN_OK (0) or a negative code; spectral_last_error
+ * returns a thread-local message for the last failure on the calling thread.
+ * Argument and shape errors are detected before anything is queued.
+ * Numerical degeneracy is reported per head through sigma and iters.
+ *
+ * Threading: a context may be used by one host thread at a time.  Distinct
+ * contexts are independent.
+ */
+#ifndef SPECTRAL_H
+#define SPECTRAL_H
+
+#include <stdint.h>
+
+#if defined(__GNUC__)
+#define SN_API __attribute__((visibility("default")))
+#else
+#define SN_API
+#endif
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SN_OK 0
+#define SN_EINVAL (-1)   /* bad shape, parameter, size or alignment            */
+#define SN_ENULL (-2)    /* a required pointer is NULL                          */
+#define SN_EDTYPE (-3)   /* dtype is neither SN_F32 nor SN_BF16                 */
+#define SN_EHIP (-4)     /* a HIP runtime call failed (message has its text)    */
+#define SN_ESTATE (-5)   /* context not usable (e.g. no device)                 */
+
+typedef enum { SN_F32 = 0, SN_BF16 = 1 } sn_dtype;
+
+typedef struct {
+  int32_t n_layers;    /* L >= 1                                                  */
+  int32_t d_model;     /* d >= 1: model width (LayerNorm/RMSNorm width, Sec. 3.1) */
+  int32_t n_q_heads;   /* n_q >= 1                                                */
+  int32_t n_kv_heads;  /* n_kv >= 1, divides n_q (n_kv == n_q: multi-head)        */
+  int32_t head_dim;    /* d_h: one of 8, 16, 32, 64, 128                          */
+  int32_t dtype;       /* sn_dtype of the weights; vectors are always float32     */
+  int64_t ld;          /* row stride of wq and wk in elements; 0 means d_model.
+                          ld * element size must be a multiple of 16 bytes.       */
+} sn_shape;
+
+typedef struct {
+  float alpha;         /* calibration factor alpha > 0 (Eq. "calibrated_bound")   */
+  float eta_fp8;       /* FP8 margin, 0 < eta_fp8 (the paper uses 0.8)            */
+  float r_max;         /* largest finite FP8 magnitude, 448 for OCP E4M3          */
+  float tol;           /* 0: run exactly n_iter iterations.  > 0: stop a head
+                          after step k >= 2 once |sigma_k - sigma_{k-1}| <=
+                          tol * sigma_k, with n_iter as the cap.                  */
+  int32_t q_strips;    /* column strips per head in the W_Q sweep; 0 = automatic  */
+  int32_t k_strips;    /* column strips per KV head in the W_K sweep; 0 = auto    */
+} sn_params;
+
+typedef struct sn_ctx sn_ctx;
+
+/* Creates a context for one model shape on the current HIP device and
+ * allocates its workspace.  hip_stream is a hipStream_t (NULL = the default
+ * stream) on which every later spectral_step is queued.  On success *ctx
+ * receives the handle.  Errors: SN_ENULL, SN_EINVAL, SN_EDTYPE, SN_EHIP. */
+SN_API int spectral_init(sn_ctx** ctx, const sn_shape* shape, const sn_params* params,
+                         void* hip_stream);
+
+/* One estimation call over all layers and heads (Sec. 4.1; App. E).
+ *   wq_layers  host array of n_layers device pointers, layer l -> wq of l
+ *              (16-byte aligned).
+ *   wk_layers  host array of n_layers device pointers to wk.
+ *   v          device float32 [n_layers][n_q][d_model], in/out: the
+ *              persistent right vectors.  Read as the start vectors (any
+ *              nonzero finite vectors; normalised on entry), overwritten with
+ *              the unit vector after the last step of each head.
+ *   u          device float32 [n_layers][n_q][d_model] or NULL: receives the
+ *              unit left vector u of each head's last step.
+ *   n_iter     >= 1: iterations (tol == 0) or the cap (tol > 0).
+ *   sigma      device float32 [n_layers][n_q]: the estimate of the last step,
+ *              sigma = ||M v|| taken before v moves.
+ *   scale      device float32 [n_layers]: Eq. "scale" with max_h sigma_h;
+ *              NaN if any head of the layer is NaN.
+ *   iters      device int32 [n_layers][n_q] or NULL: steps run per head;
+ *              -1 if the start vector is zero or not finite (sigma = NaN,
+ *              v unchanged, u = 0); -2 if M v = 0 (sigma = 0, v normalised
+ *              start vector, u = 0).
+ * The call is queued asynchronously on the context's stream.  With tol > 0
+ * it waits on the stream at iterations 2, 3, 4, 6, 9, ... to stop queueing
+ * once every head has converged.  Weights and vectors must not alias the
+ * outputs.  Errors: SN_ENULL, SN_EINVAL, SN_EHIP. */
+SN_API int spectral_step(sn_ctx* ctx, const void* const* wq_layers, const void* const* wk_layers,
+                         float* v, float* u, int32_t n_iter, float* sigma, float* scale,
+                         int32_t* iters);
+
+/* Redirects later calls to another hipStream_t. */
+SN_API int spectral_set_stream(sn_ctx* ctx, void* hip_stream);
+
+/* Frees the context and its workspace (waits for its queued work first). */
+SN_API void spectral_destroy(sn_ctx* ctx);
+
+/* Thread-local text of the last error ("" if none). */
+SN_API const char* spectral_last_error(void);
+
+/* Bytes of device workspace spectral_init allocates for this shape. */
+SN_API int spectral_workspace_bytes(const sn_shape* shape, const sn_params* params,
+                                    int64_t* bytes);
+
+/* Per-kernel timing.  With enable != 0 every later launch is bracketed by
+ * HIP events on the context's stream.  spectral_profile_read waits for the
+ * stream and returns, per kernel kind (0 = first W_K sweep from v,
+ * 1 = W_Q sweep, 2 = W_K sweep, 3 = finalize), the summed device time in
+ * milliseconds and the number of launches since the previous read, then
+ * resets both.  ms and launches point to 4 host elements each. */
+SN_API int spectral_profile(sn_ctx* ctx, int32_t enable);
+SN_API int spectral_profile_read(sn_ctx* ctx, double* ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPECTRAL_H */

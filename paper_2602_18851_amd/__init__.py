@@ -1,0 +1,23 @@
+"""MI355X-native per-head spectral norms of attention interaction matrices
+(implicit power iteration, implicit GQA) and the per-layer FP8 E4M3 scale
+of arXiv 2602.18851, behind a C ABI (include/spectral.h)."""
+
+from .spectral import (  # noqa: F401
+    EXPORTED,
+    LIB_PATH,
+    SN_BF16,
+    SN_F32,
+    Spectral,
+    SpectralError,
+    load_library,
+    sn_params,
+    sn_shape,
+    spectral_destroy,
+    spectral_init,
+    spectral_last_error,
+    spectral_profile,
+    spectral_profile_read,
+    spectral_set_stream,
+    spectral_step,
+    spectral_workspace_bytes,
+)

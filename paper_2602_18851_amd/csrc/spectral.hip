@@ -1,0 +1,847 @@
+// Per-head spectral norms of the query-key interaction matrices of every
+// attention layer by implicit power iteration, and the per-layer FP8 E4M3
+// scale factor, for MI355X (gfx950, wave64).
+//
+// Method (arXiv 2602.18851, Sec. 4.1-4.2, App. E): for query head h with key
+// head j = floor(h / g), one step is
+//     z = K_j v,  u' = Q_h^T z (= M v),  sigma = ||u'||,
+//     y = Q_h u' / sigma,  v' = K_j^T y (= M^T u),  v = v' / ||v'||,
+// where Q_h, K_j are the d_h x d row blocks of the PyTorch-layout weights
+// (the transposes of the paper's W^Q_h, W^K_j) and M = Q_h^T K_j is never
+// formed.
+//
+// Schedule.  Each step is two fused sweeps over the weights:
+//   W_Q sweep (one wave per (head, column strip)): reads every Q_h element
+//     once, computes u'[c] = sum_r Q[r,c] z[r] for the strip's columns, its
+//     squared norm, and the d_h-vector partial y[r] = sum_c Q[r,c] u'[c].
+//   W_K sweep (one wave per (KV head, chunk of <= 8 query heads, strip)):
+//     reads every K_j element once and applies it to all query heads of the
+//     chunk from registers (the implicit-GQA form of Sec. 4.2 without key
+//     expansion): v'[c] = sum_r K[r,c] y_h[r], ||v'||^2, z_h[r] partials.
+// Partials (one d_h vector and one squared norm per strip) go to a small
+// workspace and are summed, in a fixed order, by the consumer of the next
+// sweep, which also normalises (y /= sigma, z /= ||v'||).  Every reduction
+// has a fixed order, so results are bitwise reproducible run to run.
+//
+// Wave tile.  A wave covers d_h rows x (8 chunks of 16 bytes) columns:
+// lane = 8 * rg + chunk, rows rg*RPL .. rg*RPL+RPL-1 (RPL = d_h / 8),
+// columns chunk*VEC .. +VEC-1 (VEC = 8 bf16 or 4 fp32).  Each load
+// instruction reads eight full 128-byte row segments.  The column sums of the
+// first product are reduced over the 8 row groups with lane shuffles
+// (xor 8, 16, 32), the row sums of the second product accumulate in registers
+// across the whole strip and are reduced over the 8 chunks once at its end.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <string>
+#include <type_traits>
+#include <vector>
+
+#include "spectral.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define SN_HIP(expr)                                                                  \
+  do {                                                                                \
+    hipError_t e_ = (expr);                                                           \
+    if (e_ != hipSuccess)                                                             \
+      return fail(SN_EHIP, std::string(#expr) + " failed: " + hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int kWaves = 4;             // waves per workgroup
+constexpr int kThreads = 64 * kWaves;
+constexpr int kRG = 8;                // row groups per wave (lane >> 3)
+constexpr int kCPL = 8;               // 16-byte column chunks per wave row (lane & 7)
+constexpr int kMaxGC = 8;             // query heads per W_K work item
+constexpr int kQTargetItems = 16384;  // wave work items aimed for in a W_Q sweep
+constexpr int kKTargetItems = 4096;   // ... and in a W_K sweep (register-heavier waves)
+constexpr int kRsrcWord3 = 0x00020000; // buffer descriptor word 3 for gfx9-family raw loads
+
+enum { PH_INIT = 0, PH_Q = 1, PH_K = 2 };
+enum { KIND_INIT = 0, KIND_Q = 1, KIND_K = 2, KIND_FIN = 3, KIND_N = 4 };
+
+struct Work {
+  float* zp;         // [2][H][Sk][DH]  W_K-sweep partials of z, by step parity
+  float* zn;         // [2][H][Sk]      ... and of ||v'||^2 (||v||^2 for the first sweep)
+  float* yp;         // [H][Sq][DH]     W_Q-sweep partials of y
+  float* yn;         // [H][Sq]         ... and of ||u'||^2 = sigma^2
+  float* sig;        // [2][H]          sigma of the last two steps
+  float* vnorm0;     // [H]             ||v|| of the start vector
+  int32_t* alive;    // [2][H]          head continues after the step of that parity
+  int32_t* n_alive;  // [2]             heads still running after a W_K sweep
+  int32_t* iters;    // [H]             used when the caller passes no iters array
+};
+
+struct SweepArgs {
+  const void* const* mats;  // device table: per-layer wq or wk
+  int64_t ld;
+  int32_t d, n_q, n_kv, g, H;
+  int32_t s_q, s_k;         // strips of the W_Q and W_K sweeps
+  int32_t s_out, tps, n_tiles, nch, n_items;
+  int32_t k, n_iter, want_vec;
+  float tol;
+  Work w;
+  float* v;
+  float* u;
+  float* sigma;
+  int32_t* iters;
+};
+
+struct FinArgs {
+  int32_t H, L, n_q, d, s_k;
+  float coef;
+  Work w;
+  float* v;
+  float* u;
+  float* sigma;
+  float* scale;
+  int32_t* iters;
+};
+
+template <typename T>
+struct Traits;
+template <>
+struct Traits<float> {
+  static constexpr int VEC = 4;
+};
+template <>
+struct Traits<uint16_t> {  // bf16 bit patterns
+  static constexpr int VEC = 8;
+};
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // one 16-byte chunk
+
+template <typename T>
+__device__ __forceinline__ float elem(const u32x4& q, int c);
+template <>
+__device__ __forceinline__ float elem<float>(const u32x4& q, int c) {
+  return __uint_as_float(q[c]);
+}
+template <>
+__device__ __forceinline__ float elem<uint16_t>(const u32x4& q, int c) {
+  const uint32_t w = q[c >> 1];
+  return __uint_as_float((c & 1) ? (w & 0xffff0000u) : (w << 16));
+}
+
+// Marks a chunk as redefined so the compiler re-derives its float values for
+// the second product instead of keeping all of them live across the lane
+// shuffles (that would double the register footprint of a tile).
+__device__ __forceinline__ void reuse_fence(u32x4& q) { asm volatile("" : "+v"(q)); }
+
+__device__ __forceinline__ float xor_sum(float x, int m) { return x + __shfl_xor(x, m); }
+
+// Occupancy floor per SIMD: the accumulators grow with GC * DH / 8 floats.
+template <int DH, int GC>
+constexpr int waves_hint() {
+  return GC * DH / kRG >= 128 ? 2 : GC * DH / kRG >= 64 ? 3 : 4;
+}
+
+template <typename T, int DH, int GC, int PH>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_hint<DH, GC>())))
+sweep_kernel(SweepArgs a) {
+  constexpr int VEC = Traits<T>::VEC;
+  constexpr int RPL = DH / kRG;
+  constexpr int TILE_C = kCPL * VEC;
+  static_assert(DH % kRG == 0, "head_dim must be a multiple of 8");
+  __shared__ float xs[kWaves][GC][DH];
+
+  if (PH == PH_Q && blockIdx.x == 0 && threadIdx.x == 0) a.w.n_alive[a.k & 1] = 0;
+
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+  const int item = blockIdx.x * kWaves + wv;
+  const bool valid_item = item < a.n_items;
+  const int chunk = lane & 7;
+  const int rg = lane >> 3;
+  const int strip = valid_item ? item % a.s_out : 0;
+  const int rest = valid_item ? item / a.s_out : 0;
+
+  int layer, row0, head0, nvalid;
+  if (PH == PH_Q) {
+    layer = rest / a.n_q;
+    row0 = (rest % a.n_q) * DH;
+    head0 = rest;
+    nvalid = 1;
+  } else {
+    const int grp = rest / a.nch, ch = rest % a.nch;
+    layer = grp / a.n_kv;
+    const int j = grp % a.n_kv;
+    row0 = j * DH;
+    const int hin = ch * GC;
+    head0 = layer * a.n_q + j * a.g + hin;
+    nvalid = min(GC, a.g - hin);
+  }
+  if (!valid_item) nvalid = 0;
+
+  const int slot_prev = (a.k + 1) & 1;  // parity of step k-1
+  const int slot_cur = a.k & 1;
+
+  // ---- per-head decisions (wave-uniform) and normalised input vectors
+  bool act[GC], last[GC];
+  int n_cont = 0;
+#pragma unroll
+  for (int i = 0; i < GC; ++i) {
+    act[i] = false;
+    last[i] = false;
+    if (i >= nvalid) continue;
+    const int hh = head0 + i;
+    if (PH == PH_INIT) {
+      act[i] = true;
+      if (strip == 0 && lane == 0) a.w.alive[hh] = 1;  // slot 0
+      continue;
+    }
+    bool alive = a.w.alive[slot_prev * a.H + hh] != 0;
+    bool dead_v = false, dead_m = false;
+    float nv2 = 0.f;
+    if (a.k == 1) {
+      for (int s = 0; s < a.s_k; ++s) nv2 += a.w.zn[hh * a.s_k + s];
+      if (!(nv2 > 0.f) || !isfinite(nv2)) {
+        alive = false;
+        dead_v = true;
+      }
+    }
+    float inv = 0.f;
+    const float* part = nullptr;
+    int s_in = 0;
+    if (PH == PH_Q) {
+      if (alive) {
+        float n2 = 0.f;
+        for (int s = 0; s < a.s_k; ++s) n2 += a.w.zn[(slot_prev * a.H + hh) * a.s_k + s];
+        inv = 1.0f / sqrtf(n2);
+        part = a.w.zp + ((size_t)slot_prev * a.H + hh) * a.s_k * DH;
+        s_in = a.s_k;
+        act[i] = true;
+      }
+    } else {  // PH_K: sigma of this step is now complete
+      float sigma = 0.f;
+      if (alive) {
+        float s2 = 0.f;
+        for (int s = 0; s < a.s_q; ++s) s2 += a.w.yn[hh * a.s_q + s];
+        sigma = sqrtf(s2);
+        if (s2 == 0.f) {
+          dead_m = true;
+        } else {
+          act[i] = true;
+          const float prev = a.w.sig[slot_prev * a.H + hh];
+          last[i] = (a.k >= a.n_iter) ||
+                    (a.tol > 0.f && a.k >= 2 && fabsf(sigma - prev) <= a.tol * sigma);
+          inv = 1.0f / sigma;
+          part = a.w.yp + (size_t)hh * a.s_q * DH;
+          s_in = a.s_q;
+        }
+      }
+      if (strip == 0 && lane == 0) {
+        if (a.k == 1) a.w.vnorm0[hh] = sqrtf(nv2);
+        if (dead_v) {
+          a.sigma[hh] = __builtin_nanf("");
+          a.iters[hh] = -1;
+        }
+        if (dead_m) {
+          a.sigma[hh] = 0.f;
+          a.iters[hh] = -2;
+        }
+        if (act[i]) {
+          a.w.sig[slot_cur * a.H + hh] = sigma;
+          if (last[i]) {
+            a.sigma[hh] = sigma;
+            a.iters[hh] = a.k;
+          }
+        }
+        a.w.alive[slot_cur * a.H + hh] = (act[i] && !last[i]) ? 1 : 0;
+      }
+      n_cont += (act[i] && !last[i]) ? 1 : 0;
+    }
+    if (PH == PH_Q && dead_v) act[i] = false;
+    if (act[i]) {
+      for (int r = lane; r < DH; r += 64) {
+        float s = 0.f;
+        for (int t = 0; t < s_in; ++t) s += part[t * DH + r];
+        xs[wv][i][r] = s * inv;
+      }
+    }
+  }
+  if (PH == PH_K && strip == 0 && lane == 0 && n_cont > 0) atomicAdd(&a.w.n_alive[slot_cur], n_cont);
+  __syncthreads();
+
+  bool any = false;
+#pragma unroll
+  for (int i = 0; i < GC; ++i) any |= act[i];
+  if (!any) return;
+
+  // Buffer resource over this head's (or KV head's) d_h x ld row block; the
+  // hardware range check returns zeros past the last valid element, and the
+  // per-row offsets ride in scalar registers.
+  constexpr int ES = sizeof(T);
+  const char* blk = reinterpret_cast<const char*>(a.mats[layer]) + (int64_t)row0 * a.ld * ES;
+  const uint32_t nrec = (uint32_t)(((int64_t)(DH - 1) * a.ld + a.d) * ES);
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(blk), (short)0, (int)nrec, kRsrcWord3);
+  const uint32_t lane_off = (uint32_t)(((int64_t)rg * RPL * a.ld + chunk * VEC) * ES);
+  const uint32_t row_bytes = (uint32_t)(a.ld * ES);
+
+  float xr1[GC == 1 ? RPL : 1];
+  if (GC == 1 && PH != PH_INIT) {
+#pragma unroll
+    for (int rr = 0; rr < (GC == 1 ? RPL : 1); ++rr) xr1[rr] = xs[wv][0][rg * RPL + rr];
+  }
+
+  float acc[GC][RPL];
+  float nrm[GC];
+#pragma unroll
+  for (int i = 0; i < GC; ++i) {
+    nrm[i] = 0.f;
+#pragma unroll
+    for (int rr = 0; rr < RPL; ++rr) acc[i][rr] = 0.f;
+  }
+
+  const int t0 = strip * a.tps;
+  const int t1 = min(t0 + a.tps, a.n_tiles);
+  const int n_full = a.d / TILE_C;  // tiles whose columns are all inside d
+
+  // One tile: FULL tiles take unmasked 16-byte loads; the single ragged tail
+  // tile (d % TILE_C != 0) clamps every address into the row and masks.
+  auto tile_step = [&](auto full_tag, int t) {
+    constexpr bool FULL = decltype(full_tag)::value;
+    const int col = t * TILE_C + chunk * VEC;
+    const int nval = FULL ? VEC : a.d - col;
+    const uint32_t voff = lane_off + (uint32_t)(t * TILE_C * ES);
+    u32x4 tile[RPL];
+#pragma unroll
+    for (int rr = 0; rr < RPL; ++rr) tile[rr] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, rr * row_bytes, 0);
+    if (!FULL) {
+      // the ragged tail: zero the elements at columns >= d (they belong to
+      // the row's padding, to the next row, or read as 0 past the range)
+      u32x4 m;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (VEC == 8)
+          m[q] = (2 * q < nval ? 0x0000ffffu : 0u) | (2 * q + 1 < nval ? 0xffff0000u : 0u);
+        else
+          m[q] = q < nval ? 0xffffffffu : 0u;
+      }
+#pragma unroll
+      for (int rr = 0; rr < RPL; ++rr) tile[rr] &= m;
+    }
+
+#pragma unroll
+    for (int i = 0; i < GC; ++i) {
+      if (!act[i]) continue;
+      const int hh = head0 + i;
+      float w[VEC];
+      if (PH == PH_INIT) {
+        const float* vrow = a.v + (size_t)hh * a.d;
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) {
+          const float x = vrow[FULL ? col + c : min(col + c, a.d - 1)];
+          w[c] = (FULL || c < nval) ? x : 0.f;
+        }
+      } else {
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) w[c] = 0.f;
+#pragma unroll
+        for (int rr = 0; rr < RPL; ++rr) {
+          const float x = (GC == 1) ? xr1[GC == 1 ? rr : 0] : xs[wv][i][rg * RPL + rr];
+#pragma unroll
+          for (int c = 0; c < VEC; ++c) w[c] = fmaf(elem<T>(tile[rr], c), x, w[c]);
+        }
+#pragma unroll
+        for (int rr = 0; rr < RPL; ++rr) reuse_fence(tile[rr]);
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) {
+          w[c] = xor_sum(w[c], 8);
+          w[c] = xor_sum(w[c], 16);
+          w[c] = xor_sum(w[c], 32);
+        }
+      }
+#pragma unroll
+      for (int c = 0; c < VEC; ++c) nrm[i] = fmaf(w[c], w[c], nrm[i]);
+
+      // full d-space vector of the final step: v' (W_K sweep) or u' (W_Q sweep)
+      const bool write_vec = (PH == PH_K) ? last[i] : (PH == PH_Q && a.want_vec);
+      if (write_vec && rg == 0) {
+        float* out = ((PH == PH_K) ? a.v : a.u) + (size_t)hh * a.d + col;
+#pragma unroll
+        for (int c = 0; c < VEC; ++c)
+          if (FULL || c < nval) out[c] = w[c];
+      }
+      if (PH == PH_K && last[i]) continue;  // z of a finished head is not needed
+#pragma unroll
+      for (int rr = 0; rr < RPL; ++rr) {
+        float s = acc[i][rr];
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) s = fmaf(elem<T>(tile[rr], c), w[c], s);
+        acc[i][rr] = s;
+      }
+    }
+  };
+
+  const int t_full_end = min(t1, n_full);
+#pragma unroll 1
+  for (int t = t0; t < t_full_end; ++t) tile_step(std::true_type{}, t);
+  if (t1 > n_full && t1 > t0) tile_step(std::false_type{}, t1 - 1);  // the ragged last tile
+
+  // ---- reduce over the 8 column chunks and write this strip's partials
+  float* outp = (PH == PH_Q) ? a.w.yp : a.w.zp + (size_t)slot_cur * a.H * a.s_k * DH;
+  float* outn = (PH == PH_Q) ? a.w.yn : a.w.zn + (size_t)slot_cur * a.H * a.s_k;
+#pragma unroll
+  for (int i = 0; i < GC; ++i) {
+    if (!act[i]) continue;
+    const int hh = head0 + i;
+    float n = nrm[i];
+    n = xor_sum(n, 1);
+    n = xor_sum(n, 2);
+    n = xor_sum(n, 4);
+    if (lane == 0) outn[(size_t)hh * a.s_out + strip] = n;
+    if (PH == PH_K && last[i]) continue;
+    float* op = outp + ((size_t)hh * a.s_out + strip) * DH + rg * RPL;
+#pragma unroll
+    for (int rr = 0; rr < RPL; ++rr) {
+      float s = acc[i][rr];
+      s = xor_sum(s, 1);
+      s = xor_sum(s, 2);
+      s = xor_sum(s, 4);
+      if ((rr & 7) == chunk) op[rr] = s;
+    }
+  }
+}
+
+// Normalises the final vectors and computes the per-layer scale.
+// Blocks [0, H): one head each; blocks [H, H + L): one layer each.
+__global__ void __launch_bounds__(kThreads) finalize_kernel(FinArgs f) {
+  const int b = blockIdx.x;
+  if (b < f.H) {
+    const int it = f.iters[b];
+    float vs = 1.f, us = 0.f;
+    bool touch_v = false;
+    if (it > 0) {
+      float n2 = 0.f;
+      for (int s = 0; s < f.s_k; ++s) n2 += f.w.zn[((size_t)(it & 1) * f.H + b) * f.s_k + s];
+      vs = 1.0f / sqrtf(n2);
+      us = 1.0f / f.sigma[b];
+      touch_v = true;
+    } else if (it == -2) {
+      vs = 1.0f / f.w.vnorm0[b];
+      touch_v = true;
+    }
+    float* vp = f.v + (size_t)b * f.d;
+    float* up = f.u ? f.u + (size_t)b * f.d : nullptr;
+    for (int c = threadIdx.x; c < f.d; c += blockDim.x) {
+      if (touch_v) vp[c] *= vs;
+      if (up) up[c] = (it > 0) ? up[c] * us : 0.f;
+    }
+  } else {
+    const int l = b - f.H;
+    __shared__ float red[kThreads];
+    __shared__ int nan_seen;
+    if (threadIdx.x == 0) nan_seen = 0;
+    __syncthreads();
+    float m = 0.f;
+    for (int h = threadIdx.x; h < f.n_q; h += blockDim.x) {
+      const float s = f.sigma[(size_t)l * f.n_q + h];
+      if (isnan(s)) nan_seen = 1;
+      m = fmaxf(m, s);
+    }
+    red[threadIdx.x] = m;
+    __syncthreads();
+    for (int off = kThreads / 2; off > 0; off >>= 1) {
+      if ((int)threadIdx.x < off) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + off]);
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) f.scale[l] = nan_seen ? __builtin_nanf("") : f.coef * red[0];
+  }
+}
+
+// ------------------------------------------------------------------ host side
+
+struct Plan {
+  int H, g, gc, nch, vec, tile_c, n_tiles;
+  int s_q, tps_q, s_k, tps_k;
+  size_t off_zp, off_zn, off_yp, off_yn, off_sig, off_vn, off_alive, off_nalive, off_iters, bytes;
+};
+
+int esize(int dtype) { return dtype == SN_F32 ? 4 : 2; }
+
+bool supported_dh(int dh) { return dh == 8 || dh == 16 || dh == 32 || dh == 64 || dh == 128; }
+
+int validate(const sn_shape* s, const sn_params* p) {
+  if (!s || !p) return fail(SN_ENULL, "shape and params must not be NULL");
+  if (s->dtype != SN_F32 && s->dtype != SN_BF16) return fail(SN_EDTYPE, "dtype must be SN_F32 or SN_BF16");
+  if (s->n_layers < 1 || s->d_model < 1 || s->n_q_heads < 1 || s->n_kv_heads < 1 || s->head_dim < 1)
+    return fail(SN_EINVAL, "n_layers, d_model, n_q_heads, n_kv_heads and head_dim must be >= 1");
+  if (s->n_q_heads % s->n_kv_heads != 0) return fail(SN_EINVAL, "n_kv_heads must divide n_q_heads");
+  if (!supported_dh(s->head_dim)) return fail(SN_EINVAL, "head_dim must be one of 8, 16, 32, 64, 128");
+  const int64_t ld = s->ld == 0 ? s->d_model : s->ld;
+  if (ld < s->d_model) return fail(SN_EINVAL, "ld must be >= d_model");
+  if ((ld * esize(s->dtype)) % 16 != 0) return fail(SN_EINVAL, "ld * element size must be a multiple of 16 bytes");
+  const int64_t H = (int64_t)s->n_layers * s->n_q_heads;
+  if (H * (int64_t)s->d_model > (int64_t(1) << 40) || H > (1 << 26))
+    return fail(SN_EINVAL, "shape too large");
+  if (!(p->alpha > 0.f) || !(p->eta_fp8 > 0.f) || !(p->r_max > 0.f) || !std::isfinite(p->alpha) ||
+      !std::isfinite(p->eta_fp8) || !std::isfinite(p->r_max))
+    return fail(SN_EINVAL, "alpha, eta_fp8 and r_max must be finite and > 0");
+  if (!(p->tol >= 0.f) || !std::isfinite(p->tol)) return fail(SN_EINVAL, "tol must be finite and >= 0");
+  if (p->q_strips < 0 || p->k_strips < 0) return fail(SN_EINVAL, "strip counts must be >= 0");
+  return SN_OK;
+}
+
+int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+void strips(int n_tiles, int64_t units, int requested, int target, int* s_out, int* tps_out) {
+  int s = requested > 0 ? requested : ceil_div(target, std::max<int64_t>(units, 1));
+  s = std::max(1, std::min(s, n_tiles));
+  const int tps = ceil_div(n_tiles, s);
+  *tps_out = tps;
+  *s_out = ceil_div(n_tiles, tps);
+}
+
+Plan make_plan(const sn_shape* s, const sn_params* p) {
+  Plan pl{};
+  const int dh = s->head_dim;
+  pl.H = s->n_layers * s->n_q_heads;
+  pl.g = s->n_q_heads / s->n_kv_heads;
+  pl.gc = 1;
+  while (pl.gc < pl.g && pl.gc < kMaxGC) pl.gc *= 2;
+  pl.nch = ceil_div(pl.g, pl.gc);
+  pl.vec = 16 / esize(s->dtype);
+  pl.tile_c = kCPL * pl.vec;
+  pl.n_tiles = ceil_div(s->d_model, pl.tile_c);
+  strips(pl.n_tiles, pl.H, p->q_strips, kQTargetItems, &pl.s_q, &pl.tps_q);
+  strips(pl.n_tiles, (int64_t)s->n_layers * s->n_kv_heads * pl.nch, p->k_strips, kKTargetItems, &pl.s_k,
+         &pl.tps_k);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += (bytes + 255) & ~size_t(255);
+    return o;
+  };
+  const size_t H = pl.H;
+  pl.off_zp = take(2 * H * pl.s_k * dh * 4);
+  pl.off_zn = take(2 * H * pl.s_k * 4);
+  pl.off_yp = take(H * pl.s_q * dh * 4);
+  pl.off_yn = take(H * pl.s_q * 4);
+  pl.off_sig = take(2 * H * 4);
+  pl.off_vn = take(H * 4);
+  pl.off_alive = take(2 * H * 4);
+  pl.off_nalive = take(2 * 4);
+  pl.off_iters = take(H * 4);
+  pl.bytes = off;
+  return pl;
+}
+
+struct ProfRec {
+  int kind;
+  hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct sn_ctx {
+  sn_shape shape;
+  sn_params params;
+  Plan plan;
+  hipStream_t stream = nullptr;
+  int device = 0;
+  char* ws = nullptr;
+  Work w{};
+  const void** d_tab = nullptr;  // device [2L]: wq pointers then wk pointers
+  const void** h_tab = nullptr;  // pinned staging for the table copy
+  std::vector<const void*> cached;
+  hipEvent_t tab_event = nullptr;
+  int32_t* h_alive = nullptr;    // pinned readback of n_alive
+  bool prof = false;
+  std::vector<ProfRec> recs;
+  std::vector<hipEvent_t> pool;
+};
+
+namespace {
+
+hipEvent_t take_event(sn_ctx* c) {
+  if (!c->pool.empty()) {
+    hipEvent_t e = c->pool.back();
+    c->pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <typename T, int DH, int GC>
+void launch_k(int ph, dim3 grid, hipStream_t st, const SweepArgs& a) {
+  if (ph == PH_INIT)
+    sweep_kernel<T, DH, GC, PH_INIT><<<grid, kThreads, 0, st>>>(a);
+  else
+    sweep_kernel<T, DH, GC, PH_K><<<grid, kThreads, 0, st>>>(a);
+}
+
+template <typename T, int DH>
+void launch_dh(int ph, int gc, dim3 grid, hipStream_t st, const SweepArgs& a) {
+  if (ph == PH_Q) {
+    sweep_kernel<T, DH, 1, PH_Q><<<grid, kThreads, 0, st>>>(a);
+    return;
+  }
+  switch (gc) {
+    case 1: launch_k<T, DH, 1>(ph, grid, st, a); break;
+    case 2: launch_k<T, DH, 2>(ph, grid, st, a); break;
+    case 4: launch_k<T, DH, 4>(ph, grid, st, a); break;
+    default: launch_k<T, DH, 8>(ph, grid, st, a); break;
+  }
+}
+
+template <typename T>
+void launch_t(int dh, int ph, int gc, dim3 grid, hipStream_t st, const SweepArgs& a) {
+  switch (dh) {
+    case 8: launch_dh<T, 8>(ph, gc, grid, st, a); break;
+    case 16: launch_dh<T, 16>(ph, gc, grid, st, a); break;
+    case 32: launch_dh<T, 32>(ph, gc, grid, st, a); break;
+    case 64: launch_dh<T, 64>(ph, gc, grid, st, a); break;
+    default: launch_dh<T, 128>(ph, gc, grid, st, a); break;
+  }
+}
+
+int launch_sweep(sn_ctx* c, int ph, SweepArgs a) {
+  const Plan& pl = c->plan;
+  if (ph == PH_Q) {
+    a.mats = c->d_tab;
+    a.s_out = pl.s_q;
+    a.tps = pl.tps_q;
+    a.n_items = pl.H * pl.s_q;
+  } else {
+    a.mats = c->d_tab + c->shape.n_layers;
+    a.s_out = pl.s_k;
+    a.tps = pl.tps_k;
+    a.n_items = c->shape.n_layers * c->shape.n_kv_heads * pl.nch * pl.s_k;
+  }
+  const dim3 grid(ceil_div(a.n_items, kWaves));
+  ProfRec rec{ph == PH_INIT ? KIND_INIT : ph == PH_Q ? KIND_Q : KIND_K, nullptr, nullptr};
+  if (c->prof) {
+    rec.a = take_event(c);
+    rec.b = take_event(c);
+    if (!rec.a || !rec.b) return fail(SN_EHIP, "hipEventCreate failed");
+    SN_HIP(hipEventRecord(rec.a, c->stream));
+  }
+  if (c->shape.dtype == SN_BF16)
+    launch_t<uint16_t>(c->shape.head_dim, ph, pl.gc, grid, c->stream, a);
+  else
+    launch_t<float>(c->shape.head_dim, ph, pl.gc, grid, c->stream, a);
+  SN_HIP(hipGetLastError());
+  if (c->prof) {
+    SN_HIP(hipEventRecord(rec.b, c->stream));
+    c->recs.push_back(rec);
+  }
+  return SN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+SN_API const char* spectral_last_error(void) { return g_err.c_str(); }
+
+SN_API int spectral_workspace_bytes(const sn_shape* shape, const sn_params* params, int64_t* bytes) {
+  if (!bytes) return fail(SN_ENULL, "bytes must not be NULL");
+  const int rc = validate(shape, params);
+  if (rc != SN_OK) return rc;
+  *bytes = (int64_t)make_plan(shape, params).bytes;
+  return SN_OK;
+}
+
+SN_API int spectral_init(sn_ctx** ctx, const sn_shape* shape, const sn_params* params, void* hip_stream) {
+  if (!ctx) return fail(SN_ENULL, "ctx must not be NULL");
+  *ctx = nullptr;
+  const int rc = validate(shape, params);
+  if (rc != SN_OK) return rc;
+  sn_ctx* c = new sn_ctx();
+  c->shape = *shape;
+  if (c->shape.ld == 0) c->shape.ld = shape->d_model;
+  c->params = *params;
+  c->plan = make_plan(&c->shape, params);
+  c->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  auto cleanup = [&](int code) {
+    spectral_destroy(c);
+    return code;
+  };
+  if (hipGetDevice(&c->device) != hipSuccess) return cleanup(fail(SN_ESTATE, "no HIP device"));
+  const size_t L = c->shape.n_layers;
+  if (hipMalloc(&c->ws, c->plan.bytes) != hipSuccess) return cleanup(fail(SN_EHIP, "hipMalloc(workspace) failed"));
+  if (hipMalloc(&c->d_tab, 2 * L * sizeof(void*)) != hipSuccess)
+    return cleanup(fail(SN_EHIP, "hipMalloc(pointer table) failed"));
+  if (hipHostMalloc(&c->h_tab, 2 * L * sizeof(void*), hipHostMallocDefault) != hipSuccess)
+    return cleanup(fail(SN_EHIP, "hipHostMalloc(pointer table) failed"));
+  if (hipHostMalloc(&c->h_alive, 2 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess)
+    return cleanup(fail(SN_EHIP, "hipHostMalloc failed"));
+  if (hipEventCreateWithFlags(&c->tab_event, hipEventDisableTiming) != hipSuccess)
+    return cleanup(fail(SN_EHIP, "hipEventCreate failed"));
+  const Plan& pl = c->plan;
+  c->w.zp = reinterpret_cast<float*>(c->ws + pl.off_zp);
+  c->w.zn = reinterpret_cast<float*>(c->ws + pl.off_zn);
+  c->w.yp = reinterpret_cast<float*>(c->ws + pl.off_yp);
+  c->w.yn = reinterpret_cast<float*>(c->ws + pl.off_yn);
+  c->w.sig = reinterpret_cast<float*>(c->ws + pl.off_sig);
+  c->w.vnorm0 = reinterpret_cast<float*>(c->ws + pl.off_vn);
+  c->w.alive = reinterpret_cast<int32_t*>(c->ws + pl.off_alive);
+  c->w.n_alive = reinterpret_cast<int32_t*>(c->ws + pl.off_nalive);
+  c->w.iters = reinterpret_cast<int32_t*>(c->ws + pl.off_iters);
+  *ctx = c;
+  return SN_OK;
+}
+
+SN_API int spectral_set_stream(sn_ctx* c, void* hip_stream) {
+  if (!c) return fail(SN_ENULL, "ctx must not be NULL");
+  c->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  return SN_OK;
+}
+
+SN_API void spectral_destroy(sn_ctx* c) {
+  if (!c) return;
+  if (c->stream || c->ws) (void)hipStreamSynchronize(c->stream);
+  for (auto& r : c->recs) {
+    if (r.a) (void)hipEventDestroy(r.a);
+    if (r.b) (void)hipEventDestroy(r.b);
+  }
+  for (auto e : c->pool) (void)hipEventDestroy(e);
+  if (c->tab_event) (void)hipEventDestroy(c->tab_event);
+  if (c->h_alive) (void)hipHostFree(c->h_alive);
+  if (c->h_tab) (void)hipHostFree(c->h_tab);
+  if (c->d_tab) (void)hipFree(c->d_tab);
+  if (c->ws) (void)hipFree(c->ws);
+  delete c;
+}
+
+SN_API int spectral_profile(sn_ctx* c, int32_t enable) {
+  if (!c) return fail(SN_ENULL, "ctx must not be NULL");
+  c->prof = enable != 0;
+  return SN_OK;
+}
+
+SN_API int spectral_profile_read(sn_ctx* c, double* ms, int64_t* launches) {
+  if (!c || !ms || !launches) return fail(SN_ENULL, "ctx, ms and launches must not be NULL");
+  for (int k = 0; k < KIND_N; ++k) {
+    ms[k] = 0.0;
+    launches[k] = 0;
+  }
+  SN_HIP(hipStreamSynchronize(c->stream));
+  for (auto& r : c->recs) {
+    float t = 0.f;
+    SN_HIP(hipEventElapsedTime(&t, r.a, r.b));
+    ms[r.kind] += t;
+    launches[r.kind] += 1;
+    c->pool.push_back(r.a);
+    c->pool.push_back(r.b);
+  }
+  c->recs.clear();
+  return SN_OK;
+}
+
+SN_API int spectral_step(sn_ctx* c, const void* const* wq_layers, const void* const* wk_layers, float* v,
+                         float* u, int32_t n_iter, float* sigma, float* scale, int32_t* iters) {
+  if (!c) return fail(SN_ENULL, "ctx must not be NULL");
+  if (!wq_layers || !wk_layers || !v || !sigma || !scale)
+    return fail(SN_ENULL, "wq_layers, wk_layers, v, sigma and scale must not be NULL");
+  if (n_iter < 1) return fail(SN_EINVAL, "n_iter must be >= 1");
+  const int L = c->shape.n_layers;
+  for (int l = 0; l < L; ++l) {
+    if (!wq_layers[l] || !wk_layers[l]) return fail(SN_ENULL, "a layer weight pointer is NULL");
+    if ((reinterpret_cast<uintptr_t>(wq_layers[l]) | reinterpret_cast<uintptr_t>(wk_layers[l])) & 15)
+      return fail(SN_EINVAL, "layer weight pointers must be 16-byte aligned");
+  }
+  int cur_dev = 0;
+  SN_HIP(hipGetDevice(&cur_dev));
+  if (cur_dev != c->device) return fail(SN_ESTATE, "the current HIP device is not the context's device");
+
+  // device copy of the per-layer pointer table (only when it changed)
+  bool same = c->cached.size() == (size_t)(2 * L);
+  for (int l = 0; same && l < L; ++l)
+    same = c->cached[l] == wq_layers[l] && c->cached[L + l] == wk_layers[l];
+  if (!same) {
+    SN_HIP(hipEventSynchronize(c->tab_event));  // the staging buffer's previous copy has been read
+    c->cached.assign(2 * L, nullptr);
+    for (int l = 0; l < L; ++l) {
+      c->h_tab[l] = c->cached[l] = wq_layers[l];
+      c->h_tab[L + l] = c->cached[L + l] = wk_layers[l];
+    }
+    SN_HIP(hipMemcpyAsync(c->d_tab, c->h_tab, 2 * L * sizeof(void*), hipMemcpyHostToDevice, c->stream));
+    SN_HIP(hipEventRecord(c->tab_event, c->stream));
+  }
+
+  const Plan& pl = c->plan;
+  SweepArgs a{};
+  a.ld = c->shape.ld;
+  a.d = c->shape.d_model;
+  a.n_q = c->shape.n_q_heads;
+  a.n_kv = c->shape.n_kv_heads;
+  a.g = pl.g;
+  a.H = pl.H;
+  a.s_q = pl.s_q;
+  a.s_k = pl.s_k;
+  a.n_tiles = pl.n_tiles;
+  a.nch = pl.nch;
+  a.n_iter = n_iter;
+  a.tol = c->params.tol;
+  a.w = c->w;
+  a.v = v;
+  a.u = u;
+  a.sigma = sigma;
+  a.iters = iters ? iters : c->w.iters;
+
+  int rc;
+  a.k = 0;
+  if ((rc = launch_sweep(c, PH_INIT, a)) != SN_OK) return rc;
+  int next_check = 2;
+  for (int k = 1; k <= n_iter; ++k) {
+    a.k = k;
+    a.want_vec = (u != nullptr) && (c->params.tol > 0.f || k == n_iter);
+    if ((rc = launch_sweep(c, PH_Q, a)) != SN_OK) return rc;
+    a.want_vec = 0;
+    if ((rc = launch_sweep(c, PH_K, a)) != SN_OK) return rc;
+    if (c->params.tol > 0.f && k == next_check && k < n_iter) {
+      SN_HIP(hipMemcpyAsync(c->h_alive, c->w.n_alive + (k & 1), sizeof(int32_t), hipMemcpyDeviceToHost,
+                            c->stream));
+      SN_HIP(hipStreamSynchronize(c->stream));
+      if (c->h_alive[0] == 0) break;
+      next_check = k < 4 ? k + 1 : k + k / 2;
+    }
+  }
+
+  FinArgs f{};
+  f.H = pl.H;
+  f.L = L;
+  f.n_q = c->shape.n_q_heads;
+  f.d = c->shape.d_model;
+  f.s_k = pl.s_k;
+  f.coef = (float)((double)c->params.alpha * (double)c->shape.d_model /
+                   (std::sqrt((double)c->shape.head_dim) * (double)c->params.eta_fp8 * (double)c->params.r_max));
+  f.w = c->w;
+  f.v = v;
+  f.u = u;
+  f.sigma = sigma;
+  f.scale = scale;
+  f.iters = a.iters;
+  ProfRec rec{KIND_FIN, nullptr, nullptr};
+  if (c->prof) {
+    rec.a = take_event(c);
+    rec.b = take_event(c);
+    if (!rec.a || !rec.b) return fail(SN_EHIP, "hipEventCreate failed");
+    SN_HIP(hipEventRecord(rec.a, c->stream));
+  }
+  finalize_kernel<<<dim3(pl.H + L), kThreads, 0, c->stream>>>(f);
+  SN_HIP(hipGetLastError());
+  if (c->prof) {
+    SN_HIP(hipEventRecord(rec.b, c->stream));
+    c->recs.push_back(rec);
+  }
+  return SN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,236 @@
+"""ctypes binding of ``libspectral.so`` (C ABI declared in include/spectral.h).
+
+The functions named like the C entry points only marshal arguments; all
+arithmetic runs in the HIP kernels.  ``Spectral`` wraps them for torch
+tensors: torch supplies device memory and the current stream, nothing else.
+There is no fallback: if the library is missing, loading raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libspectral.so")
+
+SN_OK, SN_EINVAL, SN_ENULL, SN_EDTYPE, SN_EHIP, SN_ESTATE = 0, -1, -2, -3, -4, -5
+SN_F32, SN_BF16 = 0, 1
+KIND_NAMES = ("k_sweep_first", "q_sweep", "k_sweep", "finalize")
+
+EXPORTED = (
+    "spectral_init",
+    "spectral_step",
+    "spectral_set_stream",
+    "spectral_destroy",
+    "spectral_last_error",
+    "spectral_workspace_bytes",
+    "spectral_profile",
+    "spectral_profile_read",
+)
+
+
+class sn_shape(ctypes.Structure):
+    _fields_ = [
+        ("n_layers", ctypes.c_int32),
+        ("d_model", ctypes.c_int32),
+        ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("ld", ctypes.c_int64),
+    ]
+
+
+class sn_params(ctypes.Structure):
+    _fields_ = [
+        ("alpha", ctypes.c_float),
+        ("eta_fp8", ctypes.c_float),
+        ("r_max", ctypes.c_float),
+        ("tol", ctypes.c_float),
+        ("q_strips", ctypes.c_int32),
+        ("k_strips", ctypes.c_int32),
+    ]
+
+
+class SpectralError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"spectral error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Loads the HIP library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2602_18851_amd.build`")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    lib.spectral_init.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(sn_shape), ctypes.POINTER(sn_params), vp]
+    lib.spectral_init.restype = ctypes.c_int
+    lib.spectral_step.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp, i32, vp, vp, vp]
+    lib.spectral_step.restype = ctypes.c_int
+    lib.spectral_set_stream.argtypes = [vp, vp]
+    lib.spectral_set_stream.restype = ctypes.c_int
+    lib.spectral_destroy.argtypes = [vp]
+    lib.spectral_destroy.restype = None
+    lib.spectral_last_error.argtypes = []
+    lib.spectral_last_error.restype = ctypes.c_char_p
+    lib.spectral_workspace_bytes.argtypes = [ctypes.POINTER(sn_shape), ctypes.POINTER(sn_params),
+                                             ctypes.POINTER(i64)]
+    lib.spectral_workspace_bytes.restype = ctypes.c_int
+    lib.spectral_profile.argtypes = [vp, i32]
+    lib.spectral_profile.restype = ctypes.c_int
+    lib.spectral_profile_read.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
+    lib.spectral_profile_read.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _check(rc: int):
+    if rc != SN_OK:
+        raise SpectralError(rc, spectral_last_error())
+
+
+# ------------------------------------------------ C entry points, same names
+
+
+def spectral_last_error() -> str:
+    return load_library().spectral_last_error().decode()
+
+
+def spectral_workspace_bytes(shape: sn_shape, params: sn_params) -> int:
+    out = ctypes.c_int64(0)
+    _check(load_library().spectral_workspace_bytes(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(out)))
+    return out.value
+
+
+def spectral_init(shape: sn_shape, params: sn_params, stream: int = 0) -> int:
+    ctx = ctypes.c_void_p()
+    _check(load_library().spectral_init(ctypes.byref(ctx), ctypes.byref(shape), ctypes.byref(params),
+                                        ctypes.c_void_p(stream)))
+    return ctx.value
+
+
+def spectral_step(ctx: int, wq_ptrs: Sequence[int], wk_ptrs: Sequence[int], v: int, u: int, n_iter: int,
+                  sigma: int, scale: int, iters: int) -> None:
+    n = len(wq_ptrs)
+    wq = (ctypes.c_void_p * n)(*wq_ptrs)
+    wk = (ctypes.c_void_p * n)(*wk_ptrs)
+    _check(load_library().spectral_step(ctypes.c_void_p(ctx), wq, wk, ctypes.c_void_p(v),
+                                        ctypes.c_void_p(u or None), int(n_iter), ctypes.c_void_p(sigma),
+                                        ctypes.c_void_p(scale), ctypes.c_void_p(iters or None)))
+
+
+def spectral_set_stream(ctx: int, stream: int) -> None:
+    _check(load_library().spectral_set_stream(ctypes.c_void_p(ctx), ctypes.c_void_p(stream)))
+
+
+def spectral_destroy(ctx: int) -> None:
+    load_library().spectral_destroy(ctypes.c_void_p(ctx))
+
+
+def spectral_profile(ctx: int, enable: bool) -> None:
+    _check(load_library().spectral_profile(ctypes.c_void_p(ctx), 1 if enable else 0))
+
+
+def spectral_profile_read(ctx: int) -> dict:
+    ms = (ctypes.c_double * 4)()
+    n = (ctypes.c_int64 * 4)()
+    _check(load_library().spectral_profile_read(ctypes.c_void_p(ctx), ms, n))
+    return {KIND_NAMES[i]: (ms[i], n[i]) for i in range(4)}
+
+
+# ----------------------------------------------------------- torch wrapper
+
+
+class Spectral:
+    """One context per model shape.  ``step`` runs the estimator on the
+    current torch stream of the tensors' device."""
+
+    def __init__(self, n_layers: int, d_model: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                 dtype: str, alpha: float, eta_fp8: float = 0.8, r_max: float = 448.0, tol: float = 0.0,
+                 ld: int = 0, q_strips: int = 0, k_strips: int = 0):
+        import torch
+
+        if dtype not in ("f32", "bf16"):
+            raise ValueError("dtype must be 'f32' or 'bf16'")
+        self.torch_dtype = torch.float32 if dtype == "f32" else torch.bfloat16
+        self.shape = sn_shape(n_layers, d_model, n_q_heads, n_kv_heads, head_dim,
+                              SN_F32 if dtype == "f32" else SN_BF16, ld)
+        self.params = sn_params(alpha, eta_fp8, r_max, tol, q_strips, k_strips)
+        self._stream = torch.cuda.current_stream().cuda_stream
+        self.ctx = spectral_init(self.shape, self.params, self._stream)
+
+    @property
+    def ld(self) -> int:
+        return self.shape.ld or self.shape.d_model
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            spectral_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _layer_ptrs(self, w, rows: int) -> list[int]:
+        import torch
+
+        layers = list(w.unbind(0)) if isinstance(w, torch.Tensor) and w.dim() == 3 else list(w)
+        if len(layers) != self.shape.n_layers:
+            raise ValueError(f"expected {self.shape.n_layers} layers, got {len(layers)}")
+        ptrs = []
+        for t in layers:
+            if not t.is_cuda or t.dtype != self.torch_dtype:
+                raise ValueError(f"weights must be {self.torch_dtype} CUDA tensors")
+            if t.dim() != 2 or t.shape[0] != rows or t.shape[1] < self.shape.d_model:
+                raise ValueError(f"layer weight must be [{rows}, >= {self.shape.d_model}], got {tuple(t.shape)}")
+            if t.stride(1) != 1 or t.stride(0) != self.ld:
+                raise ValueError(f"layer weight must be row-major with row stride {self.ld}")
+            ptrs.append(t.data_ptr())
+        return ptrs
+
+    def step(self, wq, wk, v, n_iter: int, u=None, sigma=None, scale=None, iters=None):
+        """wq: [L, n_q*d_h, d] tensor or list of [n_q*d_h, d]; wk likewise with
+        n_kv; v: float32 [L, n_q, d] (in/out).  Returns (sigma, scale, iters)."""
+        import torch
+
+        s = self.shape
+        L, nq, d = s.n_layers, s.n_q_heads, s.d_model
+        wq_p = self._layer_ptrs(wq, nq * s.head_dim)
+        wk_p = self._layer_ptrs(wk, s.n_kv_heads * s.head_dim)
+        dev = v.device
+        for name, t, shp in (("v", v, (L, nq, d)), ("u", u, (L, nq, d))):
+            if t is None:
+                continue
+            if t.dtype != torch.float32 or tuple(t.shape) != shp or not t.is_contiguous() or not t.is_cuda:
+                raise ValueError(f"{name} must be a contiguous float32 CUDA tensor of shape {shp}")
+        if sigma is None:
+            sigma = torch.empty(L, nq, dtype=torch.float32, device=dev)
+        if scale is None:
+            scale = torch.empty(L, dtype=torch.float32, device=dev)
+        if iters is None:
+            iters = torch.empty(L, nq, dtype=torch.int32, device=dev)
+        stream = torch.cuda.current_stream(dev).cuda_stream
+        if stream != self._stream:
+            spectral_set_stream(self.ctx, stream)
+            self._stream = stream
+        spectral_step(self.ctx, wq_p, wk_p, v.data_ptr(), u.data_ptr() if u is not None else 0, n_iter,
+                      sigma.data_ptr(), scale.data_ptr(), iters.data_ptr())
+        return sigma, scale, iters
+
+    def profile(self, enable: bool = True):
+        spectral_profile(self.ctx, enable)
+
+    def profile_read(self) -> dict:
+        return spectral_profile_read(self.ctx)

@@ -1,0 +1,284 @@
+"""GPU path vs the float64 oracle, through the C ABI (ctypes binding).
+
+Bar: relative error <= 1e-3 on every sigma_h and every layer scale, on the
+very weight bits and start vectors the GPU consumed; iteration counts equal
+(fixed count) or within one step (tolerance mode, where fp32 and fp64 may
+cross the threshold one step apart)."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.power_iteration import head_slices, layer_scale, power_iteration, spectral_step as oracle_step
+from workloads import WORKLOADS, all_weights, layer_weights, perturb_master, layer_master, start_vectors
+
+pytestmark = pytest.mark.gpu
+
+RTOL = 1e-3
+
+if not torch.cuda.is_available():  # pragma: no cover - collected on CPU machines, skipped there
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2602_18851_amd import Spectral  # noqa: E402
+
+
+def _rel(a, b):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    return np.abs(a - b) / np.abs(b)
+
+
+def run_gpu(wl, wq, wk, v0, n_iter, tol=0.0, want_u=False, **kw):
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=tol,
+                   ld=kw.pop("ld", 0), **kw)
+    v = v0.cuda().contiguous()
+    u = torch.empty_like(v) if want_u else None
+    sigma, scale, iters = est.step(wq, wk, v, n_iter, u=u)
+    torch.cuda.synchronize()
+    out = {"sigma": sigma.cpu().double().numpy(), "scale": scale.cpu().double().numpy(),
+           "iters": iters.cpu().numpy(), "v": v.cpu().double().numpy()}
+    if want_u:
+        out["u"] = u.cpu().double().numpy()
+    est.close()
+    return out
+
+
+def check_against_oracle(wl, wq_cpu, wk_cpu, v0, n_iter, gpu, tol=0.0, want_u=False):
+    ref = oracle_step(wq_cpu, wk_cpu, v0.double().numpy(), n_iter, n_kv=wl.n_kv, head_dim=wl.head_dim,
+                      alpha=wl.alpha, tol=tol, want_u=want_u)
+    s_err = _rel(gpu["sigma"], ref["sigma"]).max()
+    c_err = _rel(gpu["scale"], ref["scale"]).max()
+    print(f"{wl.key}: max rel err sigma {s_err:.3e} scale {c_err:.3e}")
+    assert s_err <= RTOL and c_err <= RTOL
+    if tol == 0.0:
+        np.testing.assert_array_equal(gpu["iters"], ref["iters"])
+    else:
+        assert np.abs(gpu["iters"] - ref["iters"]).max() <= 1
+    # vectors: informational bar |cos| >= 1 - 1e-3 when both ran the same steps
+    same = gpu["iters"] == ref["iters"]
+    cos = np.abs(np.sum(gpu["v"] * ref["v"], axis=-1))
+    assert np.all(cos[same] >= 1 - 1e-3)
+    np.testing.assert_allclose(np.linalg.norm(gpu["v"], axis=-1), 1.0, atol=1e-5)
+    if want_u:
+        cu = np.abs(np.sum(gpu["u"] * ref["u"], axis=-1))
+        assert np.all(cu[same] >= 1 - 1e-3)
+    return ref
+
+
+def _cpu_case(wl, ld=None):
+    wq, wk = all_weights(wl, "cpu")
+    v0 = start_vectors(wl, "cpu")
+    if ld is None:
+        return wq, wk, v0, wq.cuda(), wk.cuda()
+    # padded rows: the GPU sees [rows, d] views of [rows, ld] storage
+    def pad(w):
+        p = torch.zeros(w.shape[0], w.shape[1], ld, dtype=w.dtype)
+        p[:, :, :wl.d_model] = w
+        return p.cuda()[:, :, :wl.d_model]
+    return wq, wk, v0, pad(wq), pad(wk)
+
+
+def _np(w):
+    return w.float().numpy()
+
+
+@pytest.mark.parametrize("key", ["tiny", "gpt2-small"])
+def test_fp32_configs_all_heads(key):
+    wl = WORKLOADS[key]
+    wq, wk, v0, gq, gk = _cpu_case(wl)
+    gpu = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True)
+    check_against_oracle(wl, _np(wq), _np(wk), v0, wl.n_iter, gpu, want_u=True)
+
+
+CASES = [
+    # (name, overrides, ld, strip overrides)
+    ("gqa8-bf16-d1000", dict(n_layers=2, d_model=1000, n_q=16, n_kv=2, head_dim=128, dtype="bf16"), None, {}),
+    ("gqa3-bf16-ragged", dict(n_layers=1, d_model=1001, n_q=6, n_kv=2, head_dim=32, dtype="bf16"), 1008, {}),
+    ("gqa12-f32", dict(n_layers=1, d_model=512, n_q=24, n_kv=2, head_dim=16, dtype="f32"), None, {}),
+    ("mha-f32-ragged", dict(n_layers=2, d_model=1003, n_q=3, n_kv=3, head_dim=64, dtype="f32"), 1004, {}),
+    ("mha-bf16-strips", dict(n_layers=2, d_model=2048, n_q=4, n_kv=4, head_dim=128, dtype="bf16"), None,
+     dict(q_strips=3, k_strips=5)),
+    ("gqa4-bf16-one-strip", dict(n_layers=1, d_model=768, n_q=8, n_kv=2, head_dim=64, dtype="bf16"), None,
+     dict(q_strips=1, k_strips=1)),
+    ("mqa-bf16-dh8", dict(n_layers=1, d_model=64, n_q=8, n_kv=1, head_dim=8, dtype="bf16"), None, {}),
+]
+
+
+@pytest.mark.parametrize("name,over,ld,strips", CASES, ids=[c[0] for c in CASES])
+def test_shapes_against_oracle(name, over, ld, strips):
+    wl = WORKLOADS["llama2-70b-gqa"].replace(key=name, n_iter=11, std=0.02, **over)
+    wq, wk, v0, gq, gk = _cpu_case(wl, ld)
+    gpu = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True, ld=ld or 0, **strips)
+    check_against_oracle(wl, _np(wq), _np(wk), v0, wl.n_iter, gpu, want_u=True)
+
+
+def test_tolerance_mode_on_planted_spectra():
+    wl = WORKLOADS["llama2-70b-perstep"].replace(n_layers=2, d_model=256, n_q=4, n_kv=2, head_dim=16)
+    wq, wk, v0, gq, gk = _cpu_case(wl)
+    gpu = run_gpu(wl, gq, gk, v0, 2000, tol=1e-4, want_u=True)
+    check_against_oracle(wl, _np(wq), _np(wk), v0, 2000, gpu, tol=1e-4, want_u=True)
+    assert gpu["iters"].min() >= 2 and gpu["iters"].max() < 2000
+
+
+def test_one_step_and_short_runs():
+    wl = WORKLOADS["gpt2-small"].replace(n_layers=2)
+    wq, wk, v0, gq, gk = _cpu_case(wl)
+    for n in (1, 2, 3):
+        gpu = run_gpu(wl, gq, gk, v0, n, want_u=True)
+        check_against_oracle(wl, _np(wq), _np(wk), v0, n, gpu, want_u=True)
+
+
+def test_degenerate_heads():
+    wl = WORKLOADS["llama2-70b-gqa"].replace(key="degenerate", n_layers=2, d_model=256, n_q=4, n_kv=2,
+                                             head_dim=32, n_iter=6)
+    wq, wk = all_weights(wl, "cpu")
+    wk[1, 32:64] = 0                      # layer 1, KV head 1 -> M = 0 for query heads 2, 3
+    v0 = start_vectors(wl, "cpu")
+    v0[0, 1] = 0.0                        # zero start vector
+    v0[0, 2, 5] = float("nan")            # non-finite start vector
+    gpu = run_gpu(wl, wq.cuda(), wk.cuda(), v0, wl.n_iter, want_u=True)
+    ref = oracle_step(_np(wq), _np(wk), v0.double().numpy(), wl.n_iter, n_kv=2, head_dim=32, alpha=wl.alpha,
+                      want_u=True)
+    np.testing.assert_array_equal(gpu["iters"], ref["iters"])
+    assert gpu["iters"][0, 1] == -1 and gpu["iters"][0, 2] == -1
+    assert np.isnan(gpu["sigma"][0, 1]) and np.isnan(gpu["sigma"][0, 2]) and np.isnan(gpu["scale"][0])
+    assert (gpu["iters"][1, 2:] == -2).all() and (gpu["sigma"][1, 2:] == 0).all()
+    np.testing.assert_array_equal(gpu["v"][0, 1], 0.0)               # unchanged
+    vn = v0[1, 2:].double().numpy()
+    np.testing.assert_allclose(gpu["v"][1, 2:], vn / np.linalg.norm(vn, axis=-1, keepdims=True), atol=1e-6)
+    assert not gpu["u"][0, 1:3].any() and not gpu["u"][1, 2:].any()
+    ok = gpu["iters"] > 0
+    assert _rel(gpu["sigma"][ok], ref["sigma"][ok]).max() <= RTOL
+    assert _rel(gpu["scale"][1], ref["scale"][1]) <= RTOL
+
+
+def test_bitwise_deterministic():
+    wl = WORKLOADS["llama2-70b-gqa"].replace(n_layers=2, d_model=1024, n_q=16, n_kv=2, n_iter=7)
+    wq, wk, v0, gq, gk = _cpu_case(wl)
+    a = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True)
+    b = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True)
+    for k in ("sigma", "scale", "v", "u", "iters"):
+        np.testing.assert_array_equal(a[k], b[k])
+
+
+def test_warm_start_continues_the_iteration():
+    wl = WORKLOADS["gpt2-xl"].replace(n_layers=2, n_q=5, n_kv=5)
+    wq, wk, v0, gq, gk = _cpu_case(wl)
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha)
+    v = v0.cuda()
+    est.step(gq, gk, v, 10)
+    sigma, _, _ = est.step(gq, gk, v, 10)
+    torch.cuda.synchronize()
+    ref = oracle_step(_np(wq), _np(wk), v0.double().numpy(), 20, n_kv=wl.n_kv, head_dim=wl.head_dim,
+                      alpha=wl.alpha)
+    assert _rel(sigma.cpu().numpy(), ref["sigma"]).max() <= RTOL
+    est.close()
+
+
+def test_homogeneity_of_the_gpu_path():
+    """x4 on every attention weight -> sigma and scale x16 (powers of two are exact)."""
+    wl = WORKLOADS["gpt2-xl"].replace(n_layers=2, n_q=5, n_kv=5, n_iter=8)
+    wq, wk, v0, gq, gk = _cpu_case(wl)
+    a = run_gpu(wl, gq, gk, v0, wl.n_iter)
+    b = run_gpu(wl, gq * 4, gk * 4, v0, wl.n_iter)
+    np.testing.assert_array_equal(b["sigma"], 16 * a["sigma"])
+    assert _rel(b["scale"], 16 * a["scale"]).max() < 1e-6
+
+
+# ------------------------------------------------------------- full sizes
+
+
+def _sampled_heads(wl, rng, full_layers, per_layer):
+    heads = {(l, h) for l in full_layers for h in range(wl.n_q)}
+    for l in range(wl.n_layers):
+        for h in rng.choice(wl.n_q, size=min(per_layer, wl.n_q), replace=False):
+            heads.add((l, int(h)))
+    return sorted(heads)
+
+
+def _check_sampled(wl, gq, gk, v0, n_iter, gpu, heads, tol=0.0):
+    cache = {}
+
+    def layer(l):
+        if l not in cache:
+            cache[l] = (gq[l].float().cpu().numpy(), gk[l].float().cpu().numpy())
+        return cache[l]
+
+    sig = {}
+    worst = 0.0
+    for (l, h) in heads:
+        wq_l, wk_l = layer(l)
+        WQ, WK = head_slices(wq_l, wk_l, h, wl.n_kv, wl.head_dim)
+        r = power_iteration(WQ, WK, v0[l, h].double().cpu().numpy(), n_iter, tol)
+        sig[(l, h)] = r.sigma
+        err = _rel(gpu["sigma"][l, h], r.sigma)
+        worst = max(worst, float(err))
+        assert err <= RTOL, (l, h, gpu["sigma"][l, h], r.sigma)
+        if tol == 0.0:
+            assert gpu["iters"][l, h] == r.iters
+        else:
+            assert abs(int(gpu["iters"][l, h]) - r.iters) <= 1
+        if len(cache) > 4:
+            cache.pop(next(iter(cache)))
+    for l in {l for (l, _) in heads}:
+        if all((l, h) in sig for h in range(wl.n_q)):
+            ref = layer_scale(max(sig[(l, h)] for h in range(wl.n_q)), wl.alpha, wl.d_model, wl.head_dim)
+            assert _rel(gpu["scale"][l], ref) <= RTOL
+    print(f"{wl.key}: {len(heads)} sampled heads, max rel err sigma {worst:.3e}")
+
+
+def _run_full(wl, gq, gk, v0, n_iter, tol=0.0):
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=tol)
+    v = v0.clone()
+    sigma, scale, iters = est.step(gq, gk, v, n_iter)
+    torch.cuda.synchronize()
+    out = {"sigma": sigma.cpu().double().numpy(), "scale": scale.cpu().double().numpy(),
+           "iters": iters.cpu().numpy(), "v": v}
+    est.close()
+    return out
+
+
+@pytest.mark.parametrize("key", ["gpt2-xl", "llama2-7b-spiked", "llama2-70b-gqa"])
+def test_full_size_sampled(key):
+    wl = WORKLOADS[key]
+    gq, gk = all_weights(wl, "cuda")
+    v0 = start_vectors(wl, "cuda")
+    gpu = _run_full(wl, gq, gk, v0, wl.n_iter)
+    assert np.isfinite(gpu["sigma"]).all() and (gpu["iters"] == wl.n_iter).all()
+    rng = np.random.default_rng(wl.cfg_id)
+    heads = _sampled_heads(wl, rng, [0, wl.n_layers - 1], 2)
+    _check_sampled(wl, gq, gk, v0, wl.n_iter, gpu, heads)
+    del gq, gk
+    torch.cuda.empty_cache()
+
+
+def test_full_size_per_step_recompute():
+    """Cold start to tolerance, perturb the weights, warm start from the
+    previous vectors; the oracle replays both calls itself."""
+    wl = WORKLOADS["llama2-70b-perstep"]
+    L = wl.n_layers
+    gq, gk = all_weights(wl, "cuda")
+    v0 = start_vectors(wl, "cuda")
+    est = Spectral(L, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=wl.tol)
+    v = v0.clone()
+    est.step(gq, gk, v, wl.n_iter)
+    gq1, gk1 = all_weights(wl, "cuda", perturbed=True)
+    sigma, scale, iters = est.step(gq1, gk1, v, wl.n_iter)
+    torch.cuda.synchronize()
+    it = iters.cpu().numpy()
+    assert it.max() <= 6, it.max()            # warm restarts converge in a few steps
+    rng = np.random.default_rng(5)
+    heads = _sampled_heads(wl, rng, [], 1)[:24]
+    worst = 0.0
+    for (l, h) in heads:
+        WQ0, WK0 = head_slices(gq[l].float().cpu().numpy(), gk[l].float().cpu().numpy(), h, wl.n_kv, wl.head_dim)
+        r0 = power_iteration(WQ0, WK0, v0[l, h].double().cpu().numpy(), wl.n_iter, wl.tol)
+        WQ1, WK1 = head_slices(gq1[l].float().cpu().numpy(), gk1[l].float().cpu().numpy(), h, wl.n_kv,
+                               wl.head_dim)
+        r1 = power_iteration(WQ1, WK1, r0.v, wl.n_iter, wl.tol)
+        err = _rel(sigma[l, h].item(), r1.sigma)
+        worst = max(worst, float(err))
+        assert err <= RTOL
+    print(f"per-step: {len(heads)} heads, max rel err {worst:.3e}, iters {it.min()}..{it.max()}")
+    est.close()

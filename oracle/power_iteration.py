@@ -31,7 +31,7 @@ Readings of points the paper leaves open (each listed in the design notes):
 
 from __future__ import annotations
 
-from dataclasses import dataclass
+from dataclasses import dataclass, field
 
 import numpy as np
 
@@ -42,6 +42,7 @@ class HeadResult:
     u: np.ndarray
     v: np.ndarray
     iters: int
+    history: list = field(default_factory=list)   # sigma_1 .. sigma_iters
 
 
 def head_slices(wq_layer, wk_layer, h: int, n_kv: int, head_dim: int):
@@ -68,20 +69,22 @@ def power_iteration(WQ: np.ndarray, WK: np.ndarray, v0: np.ndarray, n_iter: int,
     u = np.zeros(d)
     sigma_prev = None
     sigma = float("nan")
+    history = []
     for k in range(1, n_iter + 1):
         z = WK.T @ v
         u_p = WQ @ z
         sigma = float(np.linalg.norm(u_p))
         if sigma == 0.0:
-            return HeadResult(0.0, np.zeros(d), v0 / nv, -2)
+            return HeadResult(0.0, np.zeros(d), v0 / nv, -2, history)
+        history.append(sigma)
         u = u_p / sigma
         y = WQ.T @ u
         v_p = WK @ y
         v = v_p / np.linalg.norm(v_p)
         if tol > 0.0 and k >= 2 and abs(sigma - sigma_prev) <= tol * sigma:
-            return HeadResult(sigma, u, v, k)
+            return HeadResult(sigma, u, v, k, history)
         sigma_prev = sigma
-    return HeadResult(sigma, u, v, n_iter)
+    return HeadResult(sigma, u, v, n_iter, history)
 
 
 def repeat_blocks(z_kv: np.ndarray, g: int, head_dim: int) -> np.ndarray:

@@ -284,7 +284,10 @@ sweep_kernel(SweepArgs a) {
   // per-row offsets ride in scalar registers.
   constexpr int ES = sizeof(T);
   const char* blk = reinterpret_cast<const char*>(a.mats[layer]) + (int64_t)row0 * a.ld * ES;
-  const uint32_t nrec = (uint32_t)(((int64_t)(DH - 1) * a.ld + a.d) * ES);
+  // The range ends at the block's last valid element, rounded up to whole 16-byte
+  // chunks: the hardware drops a chunk that crosses the range end, and an aligned
+  // chunk that starts inside the matrix never leaves its memory page.
+  const uint32_t nrec = (uint32_t)((((int64_t)(DH - 1) * a.ld + a.d) * ES + 15) & ~int64_t(15));
   const __amdgpu_buffer_rsrc_t rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(blk), (short)0, (int)nrec, kRsrcWord3);
   const uint32_t lane_off = (uint32_t)(((int64_t)rg * RPL * a.ld + chunk * VEC) * ES);

@@ -40,6 +40,8 @@ def parse():
     p.add_argument("--n-iter", type=int, default=0, help="override the workload's iteration count")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle CPU baseline")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--q-strips", type=int, default=0, help="column strips per head in the W_Q sweep (0 = auto)")
+    p.add_argument("--k-strips", type=int, default=0, help="column strips per KV head in the W_K sweep (0 = auto)")
     return p.parse_args()
 
 
@@ -113,7 +115,8 @@ def main():
     sigma = torch.empty(wl.n_layers, wl.n_q, dtype=torch.float32, device=dev)
     scale = torch.empty(wl.n_layers, dtype=torch.float32, device=dev)
     iters = torch.empty(wl.n_layers, wl.n_q, dtype=torch.int32, device=dev)
-    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=0.0)
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=0.0,
+                   q_strips=args.q_strips, k_strips=args.k_strips)
     torch.cuda.synchronize()
 
     def step():

@@ -67,6 +67,7 @@ constexpr int kMaxGC = 8;             // query heads per W_K work item
 constexpr int kQTargetItems = 16384;  // wave work items aimed for in a W_Q sweep
 constexpr int kKTargetItems = 4096;   // ... and in a W_K sweep (register-heavier waves)
 constexpr int kRsrcWord3 = 0x00020000; // buffer descriptor word 3 for gfx9-family raw loads
+constexpr int kStreamPolicy = 2;       // cache policy of the weight loads: non-temporal (read once per sweep)
 
 enum { PH_INIT = 0, PH_Q = 1, PH_K = 2 };
 enum { KIND_INIT = 0, KIND_Q = 1, KIND_K = 2, KIND_FIN = 3, KIND_N = 4 };
@@ -321,7 +322,8 @@ sweep_kernel(SweepArgs a) {
     const uint32_t voff = lane_off + (uint32_t)(t * TILE_C * ES);
     u32x4 tile[RPL];
 #pragma unroll
-    for (int rr = 0; rr < RPL; ++rr) tile[rr] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, rr * row_bytes, 0);
+    for (int rr = 0; rr < RPL; ++rr)
+      tile[rr] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, rr * row_bytes, kStreamPolicy);
     if (!FULL) {
       // the ragged tail: zero the elements at columns >= d (they belong to
       // the row's padding, to the next row, or read as 0 past the range)

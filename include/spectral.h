@@ -78,7 +78,13 @@ typedef struct {
                           tol * sigma_k, with n_iter as the cap.                  */
   int32_t q_strips;    /* column strips per head in the W_Q sweep; 0 = automatic  */
   int32_t k_strips;    /* column strips per KV head in the W_K sweep; 0 = auto    */
+  int32_t flags;       /* SN_FLAG_* bits; 0 for the defaults                      */
 } sn_params;
+
+/* Run the W_K sweeps of grouped heads on the vector ALUs even where the
+ * matrix-core kernel applies (bf16 weights, d_h 64 or 128, >= 3 query heads
+ * per KV head).  Results agree to rounding; the flag exists for comparison. */
+#define SN_FLAG_VALU_K_SWEEP 1
 
 typedef struct sn_ctx sn_ctx;
 

@@ -7,6 +7,7 @@ from .spectral import (  # noqa: F401
     LIB_PATH,
     SN_BF16,
     SN_F32,
+    SN_FLAG_VALU_K_SWEEP,
     Spectral,
     SpectralError,
     load_library,

@@ -148,48 +148,49 @@ constexpr int waves_hint() {
   return GC * DH / kRG >= 128 ? 2 : GC * DH / kRG >= 64 ? 3 : 4;
 }
 
-template <typename T, int DH, int GC, int PH>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_hint<DH, GC>())))
-sweep_kernel(SweepArgs a) {
-  constexpr int VEC = Traits<T>::VEC;
-  constexpr int RPL = DH / kRG;
-  constexpr int TILE_C = kCPL * VEC;
-  static_assert(DH % kRG == 0, "head_dim must be a multiple of 8");
-  __shared__ float xs[kWaves][GC][DH];
+// Work item of a sweep: which layer, which d_h-row block of that layer's
+// matrix, and which query heads (head0 .. head0 + nvalid - 1).
+struct Item {
+  int layer, row0, head0, nvalid, strip;
+};
 
-  if (PH == PH_Q && blockIdx.x == 0 && threadIdx.x == 0) a.w.n_alive[a.k & 1] = 0;
-
-  const int lane = threadIdx.x & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-  const int item = blockIdx.x * kWaves + wv;
+template <int DH, int GC, int PH>
+__device__ __forceinline__ Item decode_item(const SweepArgs& a, int item) {
+  Item it;
   const bool valid_item = item < a.n_items;
-  const int chunk = lane & 7;
-  const int rg = lane >> 3;
-  const int strip = valid_item ? item % a.s_out : 0;
+  it.strip = valid_item ? item % a.s_out : 0;
   const int rest = valid_item ? item / a.s_out : 0;
-
-  int layer, row0, head0, nvalid;
   if (PH == PH_Q) {
-    layer = rest / a.n_q;
-    row0 = (rest % a.n_q) * DH;
-    head0 = rest;
-    nvalid = 1;
+    it.layer = rest / a.n_q;
+    it.row0 = (rest % a.n_q) * DH;
+    it.head0 = rest;
+    it.nvalid = 1;
   } else {
     const int grp = rest / a.nch, ch = rest % a.nch;
-    layer = grp / a.n_kv;
+    it.layer = grp / a.n_kv;
     const int j = grp % a.n_kv;
-    row0 = j * DH;
+    it.row0 = j * DH;
     const int hin = ch * GC;
-    head0 = layer * a.n_q + j * a.g + hin;
-    nvalid = min(GC, a.g - hin);
+    it.head0 = it.layer * a.n_q + j * a.g + hin;
+    it.nvalid = min(GC, a.g - hin);
   }
-  if (!valid_item) nvalid = 0;
+  if (!valid_item) it.nvalid = 0;
+  return it;
+}
 
+// Per-head bookkeeping at the start of a sweep (wave-uniform): which heads of
+// the item still iterate, which of them take their last step here (W_K
+// sweeps decide convergence, since sigma of the step is complete only after
+// the W_Q sweep), status / sigma / iteration outputs (written once, by the
+// strip-0 wave), and the normalised input vector of every active head, summed
+// over the producer's strips in a fixed order, into xs[i][0 .. d_h).
+template <int DH, int GC, int PH>
+__device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, int lane, float (*xs)[DH],
+                                           bool (&act)[GC], bool (&last)[GC]) {
+  const int strip = itm.strip, head0 = itm.head0, nvalid = itm.nvalid;
   const int slot_prev = (a.k + 1) & 1;  // parity of step k-1
   const int slot_cur = a.k & 1;
-
   // ---- per-head decisions (wave-uniform) and normalised input vectors
-  bool act[GC], last[GC];
   int n_cont = 0;
 #pragma unroll
   for (int i = 0; i < GC; ++i) {
@@ -268,11 +269,33 @@ sweep_kernel(SweepArgs a) {
       for (int r = lane; r < DH; r += 64) {
         float s = 0.f;
         for (int t = 0; t < s_in; ++t) s += part[t * DH + r];
-        xs[wv][i][r] = s * inv;
+        xs[i][r] = s * inv;
       }
     }
   }
   if (PH == PH_K && strip == 0 && lane == 0 && n_cont > 0) atomicAdd(&a.w.n_alive[slot_cur], n_cont);
+}
+
+template <typename T, int DH, int GC, int PH>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_hint<DH, GC>())))
+sweep_kernel(SweepArgs a) {
+  constexpr int VEC = Traits<T>::VEC;
+  constexpr int RPL = DH / kRG;
+  constexpr int TILE_C = kCPL * VEC;
+  static_assert(DH % kRG == 0, "head_dim must be a multiple of 8");
+  __shared__ float xs[kWaves][GC][DH];
+
+  if (PH == PH_Q && blockIdx.x == 0 && threadIdx.x == 0) a.w.n_alive[a.k & 1] = 0;
+
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
+  const int chunk = lane & 7;
+  const int rg = lane >> 3;
+  const Item itm = decode_item<DH, GC, PH>(a, blockIdx.x * kWaves + wv);
+  const int layer = itm.layer, row0 = itm.row0, head0 = itm.head0, strip = itm.strip;
+  const int slot_cur = a.k & 1;
+  bool act[GC], last[GC];
+  head_setup<DH, GC, PH>(a, itm, lane, xs[wv], act, last);
   __syncthreads();
 
   bool any = false;
@@ -421,6 +444,235 @@ sweep_kernel(SweepArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// W_K sweep on the matrix cores (bf16 weights, d_h in {64, 128}, groups of
+// 4..8 query heads).  With g heads sharing K_j, the sweep is a skinny dense
+// contraction: V' = K_j^T Y (d x g) and Z = K_j V' (d_h x g).  Both products
+// run as v_mfma_f32_16x16x32_bf16 with 16 "slots" = 8 heads x {hi, lo}: every
+// fp32 vector is split as x = hi + lo into two bf16 values (|x - hi - lo| <=
+// 2^-16 |x|) so the products keep ~16 significant bits while K stays in its
+// native bf16.
+//   Product 2 (contraction over columns) takes K straight from the registers
+//   it was loaded into: lane = 16 * g + s holds row s of a 16-row block and 8
+//   consecutive columns, which is the MFMA A-operand layout.
+//   Product 1 (contraction over rows) needs column fragments: the tile is
+//   written to LDS row-major and read back with ds_read_b64_tr_b16, which
+//   within each 16-lane group hands lane t element (t % 4) of source lane
+//   4j + t / 4 for j = 0..3; pointing source lane s at row k0 + s / 4,
+//   column 4 (s % 4) gives lane t rows k0 .. k0 + 3 of column t.
+//   v' (16 slots x 64 columns) goes back through LDS to reach the B-operand
+//   layout of product 2.
+// Loads of the next tile are issued before the current one is processed.
+constexpr int kMWaves = 2;                 // waves per workgroup
+constexpr int kMTileC = 64;                // columns per tile
+constexpr int kMPitch = kMTileC + 16;      // LDS row pitch of the K tile (160 B)
+constexpr int kMVPitch = kMTileC + 8;      // LDS row pitch of the split v'
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8 tr_read_8(const uint16_t* p0, const uint16_t* p1) {
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p0));
+  const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p1));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+template <int GC>
+__device__ __forceinline__ bool pick(const bool (&f)[GC], int i) {
+  bool r = false;
+#pragma unroll
+  for (int k = 0; k < GC; ++k) r |= (k == i) && f[k];
+  return r;
+}
+
+template <int DH, int PH>
+__global__ void __launch_bounds__(64 * kMWaves) ksweep_mfma_kernel(SweepArgs a) {
+  constexpr int GC = 8;
+  constexpr int RB = DH / 16;          // 16-row blocks (product-2 M blocks)
+  constexpr int KB = DH / 32;          // 32-row blocks (product-1 K blocks)
+  constexpr int CB = kMTileC / 16;     // 16-column blocks (product-1 N blocks)
+  constexpr int KC = kMTileC / 32;     // 32-column blocks (product-2 K blocks)
+  constexpr int ES = 2;
+  static_assert(DH * kMPitch * 2 >= GC * DH * 4, "input vectors alias the tile buffer");
+  __shared__ __attribute__((aligned(16))) uint16_t lds_tile[kMWaves][DH * kMPitch];
+  __shared__ __attribute__((aligned(16))) uint16_t lds_v[kMWaves][16 * kMVPitch];
+
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 4, s = lane & 15;
+  const Item itm = decode_item<DH, GC, PH>(a, blockIdx.x * kMWaves + wv);
+  const int head0 = itm.head0, strip = itm.strip;
+  const int slot_cur = a.k & 1;
+  float (*xs)[DH] = reinterpret_cast<float (*)[DH]>(&lds_tile[wv][0]);  // only until the first tile
+  bool act[GC], last[GC];
+  head_setup<DH, GC, PH>(a, itm, lane, xs, act, last);
+  __syncthreads();
+  bool any = false;
+#pragma unroll
+  for (int i = 0; i < GC; ++i) any |= act[i];
+  if (!any) return;
+
+  // heads of this lane: product-1 outputs (columns) for heads 2g, 2g+1;
+  // B-operand / partial-sum slot s = head s/2, part s%2
+  const bool act0 = pick(act, 2 * g), act1 = pick(act, 2 * g + 1);
+  const bool last0 = pick(last, 2 * g), last1 = pick(last, 2 * g + 1);
+  const bool act_s = pick(act, s >> 1), last_s = pick(last, s >> 1);
+  const bool lo_part = (s & 1) != 0;
+
+  bf16x8 a1[KB];  // Y^T fragments: slot s, rows 32 kb + 8 g + t
+  if (PH == PH_K) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const float y = act_s ? xs[s >> 1][32 * kb + 8 * g + t] : 0.f;
+        const __bf16 h = (__bf16)y;
+        a1[kb][t] = lo_part ? (__bf16)(y - (float)h) : h;
+      }
+  }
+
+  const char* blk = reinterpret_cast<const char*>(a.mats[itm.layer]) + (int64_t)itm.row0 * a.ld * ES;
+  const uint32_t nrec = (uint32_t)((((int64_t)(DH - 1) * a.ld + a.d) * ES + 15) & ~int64_t(15));
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(blk), (short)0, (int)nrec, kRsrcWord3);
+  const uint32_t lane_off = (uint32_t)(((int64_t)s * a.ld + 8 * g) * ES);
+  const uint32_t row_bytes = (uint32_t)(a.ld * ES);
+
+  auto load_tile = [&](u32x4 (&buf)[RB][KC], int t) {
+    const uint32_t voff = lane_off + (uint32_t)(t * kMTileC * ES);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc)
+        buf[rb][kc] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff + 32 * kc * ES, 16 * rb * row_bytes,
+                                                             kStreamPolicy);
+  };
+
+  f32x4 zacc[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) zacc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float nrm0 = 0.f, nrm1 = 0.f;
+  const int n_full = a.d / kMTileC;
+  const int t0 = strip * a.tps;
+  const int t1 = min(t0 + a.tps, a.n_tiles);
+  uint16_t* tl = &lds_tile[wv][0];
+  uint16_t* vl = &lds_v[wv][0];
+
+  u32x4 cur[RB][KC], nxt[RB][KC];
+  load_tile(cur, t0);
+#pragma unroll 1
+  for (int t = t0; t < t1; ++t) {
+    if (t + 1 < t1) load_tile(nxt, t + 1);
+    const int c0 = t * kMTileC;
+    if (t >= n_full) {  // the ragged last tile: zero columns >= d
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc) {
+        const int nval = a.d - (c0 + 32 * kc + 8 * g);
+        u32x4 m;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          m[q] = (2 * q < nval ? 0x0000ffffu : 0u) | (2 * q + 1 < nval ? 0xffff0000u : 0u);
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) cur[rb][kc] &= m;
+      }
+    }
+
+    bf16x8 b2[KC];
+    if (PH == PH_K) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc)
+          *reinterpret_cast<u32x4*>(tl + (16 * rb + s) * kMPitch + 32 * kc + 8 * g) = cur[rb][kc];
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        f32x4 d1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+          const uint16_t* p = tl + (32 * kb + 8 * g + (s >> 2)) * kMPitch + 16 * cb + 4 * (s & 3);
+          d1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[kb], tr_read_8(p, p + 4 * kMPitch), d1, 0, 0, 0);
+        }
+        // lane: column 16 cb + s; slots 4g .. 4g+3 = heads 2g (hi, lo), 2g+1 (hi, lo)
+        const float v0 = d1[0] + d1[1];
+        const float v1 = d1[2] + d1[3];
+        nrm0 = fmaf(v0, v0, nrm0);
+        nrm1 = fmaf(v1, v1, nrm1);
+        const int col = c0 + 16 * cb + s;
+        if (col < a.d) {
+          if (last0) a.v[(size_t)(head0 + 2 * g) * a.d + col] = v0;
+          if (last1) a.v[(size_t)(head0 + 2 * g + 1) * a.d + col] = v1;
+        }
+        const __bf16 h0 = (__bf16)v0, h1 = (__bf16)v1;
+        const __bf16 l0 = (__bf16)(v0 - (float)h0), l1 = (__bf16)(v1 - (float)h1);
+        const int c = 16 * cb + s;
+        vl[(4 * g + 0) * kMVPitch + c] = __builtin_bit_cast(uint16_t, h0);
+        vl[(4 * g + 1) * kMVPitch + c] = __builtin_bit_cast(uint16_t, l0);
+        vl[(4 * g + 2) * kMVPitch + c] = __builtin_bit_cast(uint16_t, h1);
+        vl[(4 * g + 3) * kMVPitch + c] = __builtin_bit_cast(uint16_t, l1);
+      }
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc)
+        b2[kc] = *reinterpret_cast<const bf16x8*>(vl + s * kMVPitch + 32 * kc + 8 * g);
+    } else {  // first sweep: v' is the start vector itself
+      const float* vrow = a.v + (size_t)(head0 + (s >> 1)) * a.d;
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int col = c0 + 32 * kc + 8 * g + e;
+          const float x = (act_s && col < a.d) ? vrow[min(col, a.d - 1)] : 0.f;
+          if (!lo_part) nrm0 = fmaf(x, x, nrm0);
+          const __bf16 h = (__bf16)x;
+          b2[kc][e] = lo_part ? (__bf16)(x - (float)h) : h;
+        }
+    }
+
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc)
+        zacc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, cur[rb][kc]), b2[kc],
+                                                           zacc[rb], 0, 0, 0);
+    if (t + 1 < t1) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc) cur[rb][kc] = nxt[rb][kc];
+    }
+  }
+
+  // ---- partials of this strip
+  float* zp_out = a.w.zp + (size_t)slot_cur * a.H * a.s_k * DH;
+  float* zn_out = a.w.zn + (size_t)slot_cur * a.H * a.s_k;
+  // z = hi-slot + lo-slot (lanes s, s ^ 1); even lanes own head s / 2
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) zacc[rb][j] += __shfl_xor(zacc[rb][j], 1);
+  if (!lo_part && act_s && !last_s) {
+    float* op = zp_out + ((size_t)(head0 + (s >> 1)) * a.s_out + strip) * DH + 4 * g;
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) *reinterpret_cast<f32x4*>(op + 16 * rb) = zacc[rb];
+  }
+  if (PH == PH_K) {  // lane (g, s) summed columns of heads 2g, 2g+1: reduce over s
+#pragma unroll
+    for (int m = 1; m < 16; m <<= 1) {
+      nrm0 += __shfl_xor(nrm0, m);
+      nrm1 += __shfl_xor(nrm1, m);
+    }
+    if (s == 0) {
+      if (act0) zn_out[(size_t)(head0 + 2 * g) * a.s_out + strip] = nrm0;
+      if (act1) zn_out[(size_t)(head0 + 2 * g + 1) * a.s_out + strip] = nrm1;
+    }
+  } else {  // part-0 lanes of head s/2 summed disjoint columns: reduce over g
+    nrm0 += __shfl_xor(nrm0, 16);
+    nrm0 += __shfl_xor(nrm0, 32);
+    if (g == 0 && !lo_part && act_s) zn_out[(size_t)(head0 + (s >> 1)) * a.s_out + strip] = nrm0;
+  }
+}
+
 // Normalises the final vectors and computes the per-layer scale.
 // Blocks [0, H): one head each; blocks [H, H + L): one layer each.
 __global__ void __launch_bounds__(kThreads) finalize_kernel(FinArgs f) {
@@ -471,6 +723,7 @@ __global__ void __launch_bounds__(kThreads) finalize_kernel(FinArgs f) {
 
 struct Plan {
   int H, g, gc, nch, vec, tile_c, n_tiles;
+  bool mfma_k;  // W_K sweeps on the matrix cores
   int s_q, tps_q, s_k, tps_k;
   size_t off_zp, off_zn, off_yp, off_yn, off_sig, off_vn, off_alive, off_nalive, off_iters, bytes;
 };
@@ -497,6 +750,7 @@ int validate(const sn_shape* s, const sn_params* p) {
     return fail(SN_EINVAL, "alpha, eta_fp8 and r_max must be finite and > 0");
   if (!(p->tol >= 0.f) || !std::isfinite(p->tol)) return fail(SN_EINVAL, "tol must be finite and >= 0");
   if (p->q_strips < 0 || p->k_strips < 0) return fail(SN_EINVAL, "strip counts must be >= 0");
+  if (p->flags & ~SN_FLAG_VALU_K_SWEEP) return fail(SN_EINVAL, "unknown flag bits");
   return SN_OK;
 }
 
@@ -519,7 +773,11 @@ Plan make_plan(const sn_shape* s, const sn_params* p) {
   while (pl.gc < pl.g && pl.gc < kMaxGC) pl.gc *= 2;
   pl.nch = ceil_div(pl.g, pl.gc);
   pl.vec = 16 / esize(s->dtype);
-  pl.tile_c = kCPL * pl.vec;
+  pl.mfma_k = s->dtype == SN_BF16 && (dh == 64 || dh == 128) && pl.gc >= 4 &&
+              !(p->flags & SN_FLAG_VALU_K_SWEEP);
+  // the MFMA W_K sweep tiles 64 columns, the vector sweeps 8 chunks of 16 bytes;
+  // both sweeps of a plan share one tile width (so one strip split)
+  pl.tile_c = pl.mfma_k ? kMTileC : kCPL * pl.vec;
   pl.n_tiles = ceil_div(s->d_model, pl.tile_c);
   strips(pl.n_tiles, pl.H, p->q_strips, kQTargetItems, &pl.s_q, &pl.tps_q);
   strips(pl.n_tiles, (int64_t)s->n_layers * s->n_kv_heads * pl.nch, p->k_strips, kKTargetItems, &pl.s_k,
@@ -591,10 +849,20 @@ void launch_k(int ph, dim3 grid, hipStream_t st, const SweepArgs& a) {
 }
 
 template <typename T, int DH>
-void launch_dh(int ph, int gc, dim3 grid, hipStream_t st, const SweepArgs& a) {
+void launch_dh(int ph, int gc, bool mfma, dim3 grid, hipStream_t st, const SweepArgs& a) {
   if (ph == PH_Q) {
     sweep_kernel<T, DH, 1, PH_Q><<<grid, kThreads, 0, st>>>(a);
     return;
+  }
+  if constexpr (std::is_same<T, uint16_t>::value && (DH == 64 || DH == 128)) {
+    if (mfma) {
+      const dim3 mgrid(ceil_div(a.n_items, kMWaves));
+      if (ph == PH_INIT)
+        ksweep_mfma_kernel<DH, PH_INIT><<<mgrid, 64 * kMWaves, 0, st>>>(a);
+      else
+        ksweep_mfma_kernel<DH, PH_K><<<mgrid, 64 * kMWaves, 0, st>>>(a);
+      return;
+    }
   }
   switch (gc) {
     case 1: launch_k<T, DH, 1>(ph, grid, st, a); break;
@@ -605,13 +873,13 @@ void launch_dh(int ph, int gc, dim3 grid, hipStream_t st, const SweepArgs& a) {
 }
 
 template <typename T>
-void launch_t(int dh, int ph, int gc, dim3 grid, hipStream_t st, const SweepArgs& a) {
+void launch_t(int dh, int ph, int gc, bool mfma, dim3 grid, hipStream_t st, const SweepArgs& a) {
   switch (dh) {
-    case 8: launch_dh<T, 8>(ph, gc, grid, st, a); break;
-    case 16: launch_dh<T, 16>(ph, gc, grid, st, a); break;
-    case 32: launch_dh<T, 32>(ph, gc, grid, st, a); break;
-    case 64: launch_dh<T, 64>(ph, gc, grid, st, a); break;
-    default: launch_dh<T, 128>(ph, gc, grid, st, a); break;
+    case 8: launch_dh<T, 8>(ph, gc, mfma, grid, st, a); break;
+    case 16: launch_dh<T, 16>(ph, gc, mfma, grid, st, a); break;
+    case 32: launch_dh<T, 32>(ph, gc, mfma, grid, st, a); break;
+    case 64: launch_dh<T, 64>(ph, gc, mfma, grid, st, a); break;
+    default: launch_dh<T, 128>(ph, gc, mfma, grid, st, a); break;
   }
 }
 
@@ -637,9 +905,9 @@ int launch_sweep(sn_ctx* c, int ph, SweepArgs a) {
     SN_HIP(hipEventRecord(rec.a, c->stream));
   }
   if (c->shape.dtype == SN_BF16)
-    launch_t<uint16_t>(c->shape.head_dim, ph, pl.gc, grid, c->stream, a);
+    launch_t<uint16_t>(c->shape.head_dim, ph, pl.gc, pl.mfma_k, grid, c->stream, a);
   else
-    launch_t<float>(c->shape.head_dim, ph, pl.gc, grid, c->stream, a);
+    launch_t<float>(c->shape.head_dim, ph, pl.gc, pl.mfma_k, grid, c->stream, a);
   SN_HIP(hipGetLastError());
   if (c->prof) {
     SN_HIP(hipEventRecord(rec.b, c->stream));

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(HERE, "libspectral.so")
 
 SN_OK, SN_EINVAL, SN_ENULL, SN_EDTYPE, SN_EHIP, SN_ESTATE = 0, -1, -2, -3, -4, -5
 SN_F32, SN_BF16 = 0, 1
+SN_FLAG_VALU_K_SWEEP = 1
 KIND_NAMES = ("k_sweep_first", "q_sweep", "k_sweep", "finalize")
 
 EXPORTED = (
@@ -51,6 +52,7 @@ class sn_params(ctypes.Structure):
         ("tol", ctypes.c_float),
         ("q_strips", ctypes.c_int32),
         ("k_strips", ctypes.c_int32),
+        ("flags", ctypes.c_int32),
     ]
 
 
@@ -156,7 +158,7 @@ class Spectral:
 
     def __init__(self, n_layers: int, d_model: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
                  dtype: str, alpha: float, eta_fp8: float = 0.8, r_max: float = 448.0, tol: float = 0.0,
-                 ld: int = 0, q_strips: int = 0, k_strips: int = 0):
+                 ld: int = 0, q_strips: int = 0, k_strips: int = 0, flags: int = 0):
         import torch
 
         if dtype not in ("f32", "bf16"):
@@ -164,7 +166,7 @@ class Spectral:
         self.torch_dtype = torch.float32 if dtype == "f32" else torch.bfloat16
         self.shape = sn_shape(n_layers, d_model, n_q_heads, n_kv_heads, head_dim,
                               SN_F32 if dtype == "f32" else SN_BF16, ld)
-        self.params = sn_params(alpha, eta_fp8, r_max, tol, q_strips, k_strips)
+        self.params = sn_params(alpha, eta_fp8, r_max, tol, q_strips, k_strips, flags)
         self._stream = torch.cuda.current_stream().cuda_stream
         self.ctx = spectral_init(self.shape, self.params, self._stream)
 

@@ -49,7 +49,7 @@ def _shape(**kw):
 
 
 def _params(**kw):
-    base = dict(alpha=0.02, eta_fp8=0.8, r_max=448.0, tol=0.0, q_strips=0, k_strips=0)
+    base = dict(alpha=0.02, eta_fp8=0.8, r_max=448.0, tol=0.0, q_strips=0, k_strips=0, flags=0)
     base.update(kw)
     return sp.sn_params(**base)
 

@@ -102,6 +102,13 @@ CASES = [
     ("gqa4-bf16-one-strip", dict(n_layers=1, d_model=768, n_q=8, n_kv=2, head_dim=64, dtype="bf16"), None,
      dict(q_strips=1, k_strips=1)),
     ("mqa-bf16-dh8", dict(n_layers=1, d_model=64, n_q=8, n_kv=1, head_dim=8, dtype="bf16"), None, {}),
+    # grouped W_K sweeps on the matrix cores (bf16, d_h 64/128, >= 3 heads per KV head) and their VALU twin
+    ("gqa8-bf16-valu", dict(n_layers=2, d_model=1000, n_q=16, n_kv=2, head_dim=128, dtype="bf16"), None,
+     dict(flags=1)),
+    ("gqa3-bf16-dh64-ragged", dict(n_layers=1, d_model=1001, n_q=6, n_kv=2, head_dim=64, dtype="bf16"), 1008, {}),
+    ("gqa12-bf16-dh64", dict(n_layers=2, d_model=640, n_q=24, n_kv=2, head_dim=64, dtype="bf16"), None,
+     dict(k_strips=3)),
+    ("mqa-bf16-dh128", dict(n_layers=1, d_model=384, n_q=16, n_kv=1, head_dim=128, dtype="bf16"), None, {}),
 ]
 
 

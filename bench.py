@@ -42,7 +42,23 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--q-strips", type=int, default=0, help="column strips per head in the W_Q sweep (0 = auto)")
     p.add_argument("--k-strips", type=int, default=0, help="column strips per KV head in the W_K sweep (0 = auto)")
+    p.add_argument("--mode", choices=("bench", "copy"), default="bench",
+                   help="copy: one plain device copy of --copy-bytes, the reference for HBM byte counters")
+    p.add_argument("--copy-bytes", type=int, default=4 << 30)
     return p.parse_args()
+
+
+def copy_reference(nbytes: int):
+    """One device-to-device copy of a known size: its FETCH_SIZE / WRITE_SIZE
+    counter readings calibrate the per-dispatch byte counters."""
+    import torch
+
+    src = torch.full((nbytes,), 7, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"mode": "copy", "bytes_read": nbytes, "bytes_written": nbytes}), flush=True)
 
 
 def source_hash() -> str:
@@ -99,6 +115,9 @@ def main():
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
         sys.exit(2)
+    if args.mode == "copy":
+        copy_reference(args.copy_bytes)
+        return
 
     import torch
 

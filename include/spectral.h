@@ -86,6 +86,7 @@ typedef struct {
  * per KV head).  Results agree to rounding; the flag exists for comparison. */
 #define SN_FLAG_VALU_K_SWEEP 1
 
+
 typedef struct sn_ctx sn_ctx;
 
 /* Creates a context for one model shape on the current HIP device and

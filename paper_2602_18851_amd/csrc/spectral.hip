@@ -66,6 +66,7 @@ constexpr int kCPL = 8;               // 16-byte column chunks per wave row (lan
 constexpr int kMaxGC = 8;             // query heads per W_K work item
 constexpr int kQTargetItems = 16384;  // wave work items aimed for in a W_Q sweep
 constexpr int kKTargetItems = 4096;   // ... and in a W_K sweep (register-heavier waves)
+constexpr int kKMfmaResident = 3072;  // waves of the matrix-core W_K sweep resident at once (256 CUs x 12)
 constexpr int kRsrcWord3 = 0x00020000; // buffer descriptor word 3 for gfx9-family raw loads
 constexpr int kStreamPolicy = 2;       // cache policy of the weight loads: non-temporal (read once per sweep)
 
@@ -148,6 +149,32 @@ constexpr int waves_hint() {
   return GC * DH / kRG >= 128 ? 2 : GC * DH / kRG >= 64 ? 3 : 4;
 }
 
+// Sum over the 8 row groups of a wave tile (lanes that share lane mod 8):
+// the step inside a 16-lane row is a DPP row rotation by 8 fused into the
+// add; the steps across rows are lane shuffles.  Every lane ends with the
+// same total for its column.
+__device__ __forceinline__ float group_sum(float x) {
+  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x128, 0xF, 0xF, false));
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  return x;
+}
+
+// Values that every lane of a wave computes identically (they come from the
+// same addresses) are moved to scalar registers explicitly: the compiler
+// cannot prove a load from writable memory wave-uniform, and a buffer
+// descriptor it believes divergent forces a loop around every buffer load.
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ float uni(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, x)));
+}
+__device__ __forceinline__ const char* uni(const void* p) {
+  const uint64_t v = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
+  return reinterpret_cast<const char*>(((uint64_t)hi << 32) | lo);
+}
+
 // Work item of a sweep: which layer, which d_h-row block of that layer's
 // matrix, and which query heads (head0 .. head0 + nvalid - 1).
 struct Item {
@@ -203,11 +230,12 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
       if (strip == 0 && lane == 0) a.w.alive[hh] = 1;  // slot 0
       continue;
     }
-    bool alive = a.w.alive[slot_prev * a.H + hh] != 0;
+    bool alive = uni(a.w.alive[slot_prev * a.H + hh]) != 0;
     bool dead_v = false, dead_m = false;
     float nv2 = 0.f;
     if (a.k == 1) {
       for (int s = 0; s < a.s_k; ++s) nv2 += a.w.zn[hh * a.s_k + s];
+      nv2 = uni(nv2);
       if (!(nv2 > 0.f) || !isfinite(nv2)) {
         alive = false;
         dead_v = true;
@@ -220,7 +248,7 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
       if (alive) {
         float n2 = 0.f;
         for (int s = 0; s < a.s_k; ++s) n2 += a.w.zn[(slot_prev * a.H + hh) * a.s_k + s];
-        inv = 1.0f / sqrtf(n2);
+        inv = 1.0f / sqrtf(uni(n2));
         part = a.w.zp + ((size_t)slot_prev * a.H + hh) * a.s_k * DH;
         s_in = a.s_k;
         act[i] = true;
@@ -230,12 +258,13 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
       if (alive) {
         float s2 = 0.f;
         for (int s = 0; s < a.s_q; ++s) s2 += a.w.yn[hh * a.s_q + s];
+        s2 = uni(s2);
         sigma = sqrtf(s2);
         if (s2 == 0.f) {
           dead_m = true;
         } else {
           act[i] = true;
-          const float prev = a.w.sig[slot_prev * a.H + hh];
+          const float prev = uni(a.w.sig[slot_prev * a.H + hh]);
           last[i] = (a.k >= a.n_iter) ||
                     (a.tol > 0.f && a.k >= 2 && fabsf(sigma - prev) <= a.tol * sigma);
           inv = 1.0f / sigma;
@@ -280,8 +309,9 @@ template <typename T, int DH, int GC, int PH>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_hint<DH, GC>())))
 sweep_kernel(SweepArgs a) {
   constexpr int VEC = Traits<T>::VEC;
+  constexpr int CPL = kCPL;  // 16-byte column chunks per wave row: 128-byte row segments
   constexpr int RPL = DH / kRG;
-  constexpr int TILE_C = kCPL * VEC;
+  constexpr int TILE_C = CPL * VEC;
   static_assert(DH % kRG == 0, "head_dim must be a multiple of 8");
   __shared__ float xs[kWaves][GC][DH];
 
@@ -289,8 +319,8 @@ sweep_kernel(SweepArgs a) {
 
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-  const int chunk = lane & 7;
-  const int rg = lane >> 3;
+  const int chunk = lane % CPL;
+  const int rg = lane / CPL;
   const Item itm = decode_item<DH, GC, PH>(a, blockIdx.x * kWaves + wv);
   const int layer = itm.layer, row0 = itm.row0, head0 = itm.head0, strip = itm.strip;
   const int slot_cur = a.k & 1;
@@ -307,7 +337,7 @@ sweep_kernel(SweepArgs a) {
   // hardware range check returns zeros past the last valid element, and the
   // per-row offsets ride in scalar registers.
   constexpr int ES = sizeof(T);
-  const char* blk = reinterpret_cast<const char*>(a.mats[layer]) + (int64_t)row0 * a.ld * ES;
+  const char* blk = uni(a.mats[layer]) + (int64_t)row0 * a.ld * ES;
   // The range ends at the block's last valid element, rounded up to whole 16-byte
   // chunks: the hardware drops a chunk that crosses the range end, and an aligned
   // chunk that starts inside the matrix never leaves its memory page.
@@ -332,21 +362,22 @@ sweep_kernel(SweepArgs a) {
     for (int rr = 0; rr < RPL; ++rr) acc[i][rr] = 0.f;
   }
 
-  const int t0 = strip * a.tps;
-  const int t1 = min(t0 + a.tps, a.n_tiles);
   const int n_full = a.d / TILE_C;  // tiles whose columns are all inside d
+  const int t_first = strip * a.tps;
+  const int t_last = min(t_first + a.tps, a.n_tiles);  // exclusive
+  const int t_full_end = min(t_last, n_full);
+  const bool has_tail = t_last > n_full;               // the ragged last tile is ours
 
-  // One tile: FULL tiles take unmasked 16-byte loads; the single ragged tail
-  // tile (d % TILE_C != 0) clamps every address into the row and masks.
-  auto tile_step = [&](auto full_tag, int t) {
-    constexpr bool FULL = decltype(full_tag)::value;
-    const int col = t * TILE_C + chunk * VEC;
-    const int nval = FULL ? VEC : a.d - col;
+  auto load_tile = [&](u32x4 (&tile)[RPL], int t) {
     const uint32_t voff = lane_off + (uint32_t)(t * TILE_C * ES);
-    u32x4 tile[RPL];
 #pragma unroll
     for (int rr = 0; rr < RPL; ++rr)
       tile[rr] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, rr * row_bytes, kStreamPolicy);
+  };
+  auto tile_step = [&](auto full_tag, int t, u32x4 (&tile)[RPL]) {
+    constexpr bool FULL = decltype(full_tag)::value;
+    const int col = t * TILE_C + chunk * VEC;
+    const int nval = FULL ? VEC : a.d - col;
     if (!FULL) {
       // the ragged tail: zero the elements at columns >= d (they belong to
       // the row's padding, to the next row, or read as 0 past the range)
@@ -386,11 +417,7 @@ sweep_kernel(SweepArgs a) {
 #pragma unroll
         for (int rr = 0; rr < RPL; ++rr) reuse_fence(tile[rr]);
 #pragma unroll
-        for (int c = 0; c < VEC; ++c) {
-          w[c] = xor_sum(w[c], 8);
-          w[c] = xor_sum(w[c], 16);
-          w[c] = xor_sum(w[c], 32);
-        }
+        for (int c = 0; c < VEC; ++c) w[c] = group_sum(w[c]);
       }
 #pragma unroll
       for (int c = 0; c < VEC; ++c) nrm[i] = fmaf(w[c], w[c], nrm[i]);
@@ -414,10 +441,17 @@ sweep_kernel(SweepArgs a) {
     }
   };
 
-  const int t_full_end = min(t1, n_full);
 #pragma unroll 1
-  for (int t = t0; t < t_full_end; ++t) tile_step(std::true_type{}, t);
-  if (t1 > n_full && t1 > t0) tile_step(std::false_type{}, t1 - 1);  // the ragged last tile
+  for (int t = t_first; t < t_full_end; ++t) {
+    u32x4 cur[RPL];
+    load_tile(cur, t);
+    tile_step(std::true_type{}, t, cur);
+  }
+  if (has_tail) {  // the ragged last tile
+    u32x4 cur[RPL];
+    load_tile(cur, n_full);
+    tile_step(std::false_type{}, n_full, cur);
+  }
 
   // ---- reduce over the 8 column chunks and write this strip's partials
   float* outp = (PH == PH_Q) ? a.w.yp : a.w.zp + (size_t)slot_cur * a.H * a.s_k * DH;
@@ -426,20 +460,18 @@ sweep_kernel(SweepArgs a) {
   for (int i = 0; i < GC; ++i) {
     if (!act[i]) continue;
     const int hh = head0 + i;
-    float n = nrm[i];
-    n = xor_sum(n, 1);
-    n = xor_sum(n, 2);
-    n = xor_sum(n, 4);
+    float n = nrm[i];  // row group 0's copy of the column sums
+#pragma unroll
+    for (int m = 1; m < CPL; m <<= 1) n = xor_sum(n, m);
     if (lane == 0) outn[(size_t)hh * a.s_out + strip] = n;
     if (PH == PH_K && last[i]) continue;
     float* op = outp + ((size_t)hh * a.s_out + strip) * DH + rg * RPL;
 #pragma unroll
     for (int rr = 0; rr < RPL; ++rr) {
       float s = acc[i][rr];
-      s = xor_sum(s, 1);
-      s = xor_sum(s, 2);
-      s = xor_sum(s, 4);
-      if ((rr & 7) == chunk) op[rr] = s;
+#pragma unroll
+      for (int m = 1; m < CPL; m <<= 1) s = xor_sum(s, m);
+      if ((rr % CPL) == chunk) op[rr] = s;
     }
   }
 }
@@ -462,10 +494,11 @@ sweep_kernel(SweepArgs a) {
 //   column 4 (s % 4) gives lane t rows k0 .. k0 + 3 of column t.
 //   v' (16 slots x 64 columns) goes back through LDS to reach the B-operand
 //   layout of product 2.
-// Loads of the next tile are issued before the current one is processed.
+// The tile goes through LDS in two 64-row halves, which keeps a 2-wave
+// workgroup at 23 KB of LDS and 12 waves per CU in flight.
 constexpr int kMWaves = 2;                 // waves per workgroup
-constexpr int kMTileC = 64;                // columns per tile
-constexpr int kMPitch = kMTileC + 16;      // LDS row pitch of the K tile (160 B)
+constexpr int kMTileC = 64;                // columns per tile: 128-byte row segments per load
+constexpr int kMPitch = kMTileC + 8;       // LDS row pitch of the K tile (144 B: 16-lane store passes conflict-free)
 constexpr int kMVPitch = kMTileC + 8;      // LDS row pitch of the split v'
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -488,15 +521,18 @@ __device__ __forceinline__ bool pick(const bool (&f)[GC], int i) {
 }
 
 template <int DH, int PH>
-__global__ void __launch_bounds__(64 * kMWaves) ksweep_mfma_kernel(SweepArgs a) {
+__global__ void __launch_bounds__(64 * kMWaves) __attribute__((amdgpu_waves_per_eu(3)))
+ksweep_mfma_kernel(SweepArgs a) {
   constexpr int GC = 8;
   constexpr int RB = DH / 16;          // 16-row blocks (product-2 M blocks)
   constexpr int KB = DH / 32;          // 32-row blocks (product-1 K blocks)
   constexpr int CB = kMTileC / 16;     // 16-column blocks (product-1 N blocks)
   constexpr int KC = kMTileC / 32;     // 32-column blocks (product-2 K blocks)
   constexpr int ES = 2;
-  static_assert(DH * kMPitch * 2 >= GC * DH * 4, "input vectors alias the tile buffer");
-  __shared__ __attribute__((aligned(16))) uint16_t lds_tile[kMWaves][DH * kMPitch];
+  constexpr int SR = DH < 64 ? DH : 64;  // rows staged in LDS at a time (product 1 runs per half)
+  constexpr int NHALF = DH / SR;
+  static_assert(SR * kMPitch * 2 >= GC * DH * 4, "input vectors alias the tile buffer");
+  __shared__ __attribute__((aligned(16))) uint16_t lds_tile[kMWaves][SR * kMPitch];
   __shared__ __attribute__((aligned(16))) uint16_t lds_v[kMWaves][16 * kMVPitch];
 
   const int lane = threadIdx.x & 63;
@@ -533,7 +569,7 @@ __global__ void __launch_bounds__(64 * kMWaves) ksweep_mfma_kernel(SweepArgs a) 
       }
   }
 
-  const char* blk = reinterpret_cast<const char*>(a.mats[itm.layer]) + (int64_t)itm.row0 * a.ld * ES;
+  const char* blk = uni(a.mats[itm.layer]) + (int64_t)itm.row0 * a.ld * ES;
   const uint32_t nrec = (uint32_t)((((int64_t)(DH - 1) * a.ld + a.d) * ES + 15) & ~int64_t(15));
   const __amdgpu_buffer_rsrc_t rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(blk), (short)0, (int)nrec, kRsrcWord3);
@@ -556,15 +592,14 @@ __global__ void __launch_bounds__(64 * kMWaves) ksweep_mfma_kernel(SweepArgs a) 
   float nrm0 = 0.f, nrm1 = 0.f;
   const int n_full = a.d / kMTileC;
   const int t0 = strip * a.tps;
-  const int t1 = min(t0 + a.tps, a.n_tiles);
+  const int t1 = min(t0 + a.tps, a.n_tiles);  // exclusive
   uint16_t* tl = &lds_tile[wv][0];
   uint16_t* vl = &lds_v[wv][0];
 
-  u32x4 cur[RB][KC], nxt[RB][KC];
-  load_tile(cur, t0);
 #pragma unroll 1
   for (int t = t0; t < t1; ++t) {
-    if (t + 1 < t1) load_tile(nxt, t + 1);
+    u32x4 cur[RB][KC];
+    load_tile(cur, t);
     const int c0 = t * kMTileC;
     if (t >= n_full) {  // the ragged last tile: zero columns >= d
 #pragma unroll
@@ -581,22 +616,30 @@ __global__ void __launch_bounds__(64 * kMWaves) ksweep_mfma_kernel(SweepArgs a) 
 
     bf16x8 b2[KC];
     if (PH == PH_K) {
+      f32x4 d1[CB];
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
+      for (int cb = 0; cb < CB; ++cb) d1[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kc = 0; kc < KC; ++kc)
-          *reinterpret_cast<u32x4*>(tl + (16 * rb + s) * kMPitch + 32 * kc + 8 * g) = cur[rb][kc];
+      for (int hf = 0; hf < NHALF; ++hf) {  // rows hf*SR .. hf*SR+SR-1 through LDS
+#pragma unroll
+        for (int rb = 0; rb < SR / 16; ++rb)
+#pragma unroll
+          for (int kc = 0; kc < KC; ++kc)
+            *reinterpret_cast<u32x4*>(tl + (16 * rb + s) * kMPitch + 32 * kc + 8 * g) = cur[hf * (SR / 16) + rb][kc];
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int kb = 0; kb < SR / 32; ++kb) {
+            const uint16_t* p = tl + (32 * kb + 8 * g + (s >> 2)) * kMPitch + 16 * cb + 4 * (s & 3);
+            d1[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[hf * (SR / 32) + kb], tr_read_8(p, p + 4 * kMPitch),
+                                                             d1[cb], 0, 0, 0);
+          }
+      }
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb) {
-        f32x4 d1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
-          const uint16_t* p = tl + (32 * kb + 8 * g + (s >> 2)) * kMPitch + 16 * cb + 4 * (s & 3);
-          d1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[kb], tr_read_8(p, p + 4 * kMPitch), d1, 0, 0, 0);
-        }
         // lane: column 16 cb + s; slots 4g .. 4g+3 = heads 2g (hi, lo), 2g+1 (hi, lo)
-        const float v0 = d1[0] + d1[1];
-        const float v1 = d1[2] + d1[3];
+        const float v0 = d1[cb][0] + d1[cb][1];
+        const float v1 = d1[cb][2] + d1[cb][3];
         nrm0 = fmaf(v0, v0, nrm0);
         nrm1 = fmaf(v1, v1, nrm1);
         const int col = c0 + 16 * cb + s;
@@ -635,12 +678,6 @@ __global__ void __launch_bounds__(64 * kMWaves) ksweep_mfma_kernel(SweepArgs a) 
       for (int kc = 0; kc < KC; ++kc)
         zacc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, cur[rb][kc]), b2[kc],
                                                            zacc[rb], 0, 0, 0);
-    if (t + 1 < t1) {
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int kc = 0; kc < KC; ++kc) cur[rb][kc] = nxt[rb][kc];
-    }
   }
 
   // ---- partials of this strip
@@ -722,7 +759,8 @@ __global__ void __launch_bounds__(kThreads) finalize_kernel(FinArgs f) {
 // ------------------------------------------------------------------ host side
 
 struct Plan {
-  int H, g, gc, nch, vec, tile_c, n_tiles;
+  int H, g, gc, nch, vec, tile_c, n_tiles;   // W_K sweeps
+  int tile_cq, n_tiles_q;                    // W_Q sweep
   bool mfma_k;  // W_K sweeps on the matrix cores
   int s_q, tps_q, s_k, tps_k;
   size_t off_zp, off_zn, off_yp, off_yn, off_sig, off_vn, off_alive, off_nalive, off_iters, bytes;
@@ -756,8 +794,11 @@ int validate(const sn_shape* s, const sn_params* p) {
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
-void strips(int n_tiles, int64_t units, int requested, int target, int* s_out, int* tps_out) {
-  int s = requested > 0 ? requested : ceil_div(target, std::max<int64_t>(units, 1));
+// Column strips per unit (head or KV head): the request if given, else about
+// target / units (rounded up, or down when all waves should be resident at once).
+void strips(int n_tiles, int64_t units, int requested, int target, bool round_down, int* s_out, int* tps_out) {
+  const int64_t u = std::max<int64_t>(units, 1);
+  int s = requested > 0 ? requested : round_down ? (int)std::max<int64_t>(1, target / u) : ceil_div(target, u);
   s = std::max(1, std::min(s, n_tiles));
   const int tps = ceil_div(n_tiles, s);
   *tps_out = tps;
@@ -779,9 +820,11 @@ Plan make_plan(const sn_shape* s, const sn_params* p) {
   // both sweeps of a plan share one tile width (so one strip split)
   pl.tile_c = pl.mfma_k ? kMTileC : kCPL * pl.vec;
   pl.n_tiles = ceil_div(s->d_model, pl.tile_c);
-  strips(pl.n_tiles, pl.H, p->q_strips, kQTargetItems, &pl.s_q, &pl.tps_q);
-  strips(pl.n_tiles, (int64_t)s->n_layers * s->n_kv_heads * pl.nch, p->k_strips, kKTargetItems, &pl.s_k,
-         &pl.tps_k);
+  pl.tile_cq = kCPL * pl.vec;
+  pl.n_tiles_q = ceil_div(s->d_model, pl.tile_cq);
+  strips(pl.n_tiles_q, pl.H, p->q_strips, kQTargetItems, false, &pl.s_q, &pl.tps_q);
+  strips(pl.n_tiles, (int64_t)s->n_layers * s->n_kv_heads * pl.nch, p->k_strips,
+         pl.mfma_k ? kKMfmaResident : kKTargetItems, pl.mfma_k, &pl.s_k, &pl.tps_k);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -889,11 +932,13 @@ int launch_sweep(sn_ctx* c, int ph, SweepArgs a) {
     a.mats = c->d_tab;
     a.s_out = pl.s_q;
     a.tps = pl.tps_q;
+    a.n_tiles = pl.n_tiles_q;
     a.n_items = pl.H * pl.s_q;
   } else {
     a.mats = c->d_tab + c->shape.n_layers;
     a.s_out = pl.s_k;
     a.tps = pl.tps_k;
+    a.n_tiles = pl.n_tiles;
     a.n_items = c->shape.n_layers * c->shape.n_kv_heads * pl.nch * pl.s_k;
   }
   const dim3 grid(ceil_div(a.n_items, kWaves));

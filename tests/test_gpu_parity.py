@@ -109,6 +109,8 @@ CASES = [
     ("gqa12-bf16-dh64", dict(n_layers=2, d_model=640, n_q=24, n_kv=2, head_dim=64, dtype="bf16"), None,
      dict(k_strips=3)),
     ("mqa-bf16-dh128", dict(n_layers=1, d_model=384, n_q=16, n_kv=1, head_dim=128, dtype="bf16"), None, {}),
+    ("gqa4-bf16-dh64-ragged-strips", dict(n_layers=1, d_model=1001, n_q=8, n_kv=2, head_dim=64, dtype="bf16"), 1008,
+     dict(q_strips=2, k_strips=3)),
 ]
 
 
@@ -264,14 +266,18 @@ def test_full_size_sampled(key):
     torch.cuda.empty_cache()
 
 
-def _check_tolerance_stop(res_gpu_iters, res_gpu_sigma, WQ, WK, v_start, tol, cap, eps=0.02):
+def _check_tolerance_stop(res_gpu_iters, res_gpu_sigma, WQ, WK, v_start, tol, cap, eps=0.1):
     """Tolerance mode has several correct results near the threshold: the
     sigma sequence is unique, the stopping step is not, since fp32 and fp64
     may fall on either side of |sigma_k - sigma_{k-1}| <= tol sigma_k when the
     change sits at the threshold.  Checks, against the oracle's own sequence
     from the same start vector, that the GPU's sigma is the sequence's value
-    at the GPU's step k, that step k meets the rule (up to eps of the
-    threshold, fp32 noise) and that no earlier step met it by more than eps.
+    at the GPU's step k, that step k meets the rule up to eps of the threshold
+    and that no earlier step met it by more than eps.  eps comes from the GPU
+    path's precision: sigma carries about 1e-6 relative error (fp32
+    accumulation, hi/lo bf16 vector halves on the matrix cores), so the
+    difference of two estimates carries about 2e-6 sigma, i.e. 2% of
+    tol * sigma at tol = 1e-4; eps = 10% keeps a 5x margin.
     Returns the oracle's own tolerance-mode result."""
     r = power_iteration(WQ, WK, v_start, cap, tol)
     k = int(res_gpu_iters)

@@ -145,6 +145,34 @@ SN_API int spectral_workspace_bytes(const sn_shape* shape, const sn_params* para
 SN_API int spectral_profile(sn_ctx* ctx, int32_t enable);
 SN_API int spectral_profile_read(sn_ctx* ctx, double* ms, int64_t* launches);
 
+/* ---- host-side calibration helpers (no GPU involved) ------------------
+ *
+ * spectral_alpha_select: the selection rule of Sec. 3.2.  gamma is the
+ * smallest gamma > 1 with gamma - 1 - ln(gamma) >= (2 / d_h) ln(2 N L / delta)
+ * (Eq. "gamma_selection"), and alpha_min = sqrt(2 gamma d_h) / d *
+ * sqrt(ln(4 N L^2 / delta)) (Eq. "alpha_selection"), with N = n_heads_total
+ * (layers x query heads) and L = seq_len.  Writes both to host doubles.
+ * Errors: SN_ENULL, SN_EINVAL (sizes < 1, delta outside (0, 1)). */
+SN_API int spectral_alpha_select(int32_t d_model, int32_t head_dim, int64_t n_heads_total, int64_t seq_len,
+                                 double delta, double* gamma, double* alpha_min);
+
+/* T1 = L exp(-(d_h / 2)(gamma - 1 - ln gamma)), T2 = 2 L^2 exp(-d^2 alpha^2 /
+ * (2 gamma d_h)) of Prop. "Rank-aware overflow probability bound", for one
+ * head.  Errors: SN_ENULL, SN_EINVAL (alpha <= 0, gamma <= 1, sizes < 1). */
+SN_API int spectral_overflow_terms(int32_t d_model, int32_t head_dim, int64_t seq_len, double alpha,
+                                   double gamma, double* t1, double* t2);
+
+/* Auto-alpha (Sec. 3.5, App. M): alpha = Quantile_q(slack) * kappa over n
+ * burn-in slack ratios (host array), the quantile interpolating linearly
+ * between order statistics at position q (n - 1).  Errors: SN_ENULL,
+ * SN_EINVAL (n < 1, q outside [0, 1], kappa < 1, a negative or non-finite
+ * ratio). */
+SN_API int spectral_auto_alpha(const double* slack, int64_t n, double quantile, double kappa, double* alpha);
+
+/* Slack ratio r = max|S| / B_max with B_max = sigma_layer * d / sqrt(d_h)
+ * (Sec. 3.5, Eq. "bound"). */
+SN_API double spectral_slack_ratio(double max_abs_logit, double sigma_layer, int32_t d_model, int32_t head_dim);
+
 #ifdef __cplusplus
 }
 #endif

@@ -60,3 +60,22 @@ def overflow_terms(d: int, head_dim: int, seq_len: int, alpha: float, gamma: flo
 def rank_aware_improvement(d: int, head_dim: int, gamma: float) -> float:
     """Exponent ratio d / (gamma d_h) of Table "concentration"."""
     return d / (gamma * head_dim)
+
+
+def slack_ratio(max_abs_logit: float, sigma_layer: float, d: int, head_dim: int) -> float:
+    """r_t = max|S| / B_max (Sec. 3.5), B_max = sigma * d / sqrt(d_h) (Eq. "bound")."""
+    return max_abs_logit / (sigma_layer * d / math.sqrt(head_dim))
+
+
+def auto_alpha(slack_ratios, quantile: float = 0.9999, kappa: float = 1.0) -> float:
+    """Algorithm "Auto-alpha Calibration" (App. M): Quantile_q(R) * kappa.
+    The quantile is numpy's default (linear interpolation between order
+    statistics); the paper does not name an estimator."""
+    import numpy as np
+
+    return float(np.quantile(np.asarray(slack_ratios, dtype=np.float64), quantile)) * kappa
+
+
+def utilization(max_abs_logit: float, scale: float, r_max: float = 448.0) -> float:
+    """FP8 range utilisation max|S| / (scale * R_max) (Sec. 1, "Utilization")."""
+    return max_abs_logit / (scale * r_max)

@@ -13,7 +13,11 @@ from .spectral import (  # noqa: F401
     load_library,
     sn_params,
     sn_shape,
+    spectral_alpha_select,
+    spectral_auto_alpha,
     spectral_destroy,
+    spectral_overflow_terms,
+    spectral_slack_ratio,
     spectral_init,
     spectral_last_error,
     spectral_profile,

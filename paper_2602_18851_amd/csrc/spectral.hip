@@ -852,6 +852,9 @@ struct ProfRec {
 
 }  // namespace
 
+// Shared with the host-side calibration helpers (calibration.cpp).
+void sn_set_last_error(const char* msg) { g_err = msg; }
+
 struct sn_ctx {
   sn_shape shape;
   sn_params params;

@@ -29,6 +29,10 @@ EXPORTED = (
     "spectral_workspace_bytes",
     "spectral_profile",
     "spectral_profile_read",
+    "spectral_alpha_select",
+    "spectral_overflow_terms",
+    "spectral_auto_alpha",
+    "spectral_slack_ratio",
 )
 
 
@@ -91,6 +95,15 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.spectral_profile.restype = ctypes.c_int
     lib.spectral_profile_read.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]
     lib.spectral_profile_read.restype = ctypes.c_int
+    dp = ctypes.POINTER(ctypes.c_double)
+    lib.spectral_alpha_select.argtypes = [i32, i32, i64, i64, ctypes.c_double, dp, dp]
+    lib.spectral_alpha_select.restype = ctypes.c_int
+    lib.spectral_overflow_terms.argtypes = [i32, i32, i64, ctypes.c_double, ctypes.c_double, dp, dp]
+    lib.spectral_overflow_terms.restype = ctypes.c_int
+    lib.spectral_auto_alpha.argtypes = [dp, i64, ctypes.c_double, ctypes.c_double, dp]
+    lib.spectral_auto_alpha.restype = ctypes.c_int
+    lib.spectral_slack_ratio.argtypes = [ctypes.c_double, ctypes.c_double, i32, i32]
+    lib.spectral_slack_ratio.restype = ctypes.c_double
     _lib = lib
     return lib
 
@@ -147,6 +160,37 @@ def spectral_profile_read(ctx: int) -> dict:
     n = (ctypes.c_int64 * 4)()
     _check(load_library().spectral_profile_read(ctypes.c_void_p(ctx), ms, n))
     return {KIND_NAMES[i]: (ms[i], n[i]) for i in range(4)}
+
+
+# ------------------------------------------------ host calibration helpers
+
+
+def spectral_alpha_select(d_model: int, head_dim: int, n_heads_total: int, seq_len: int,
+                          delta: float) -> tuple[float, float]:
+    """(gamma, alpha_min) of the selection rule (Sec. 3.2)."""
+    g, a = ctypes.c_double(), ctypes.c_double()
+    _check(load_library().spectral_alpha_select(d_model, head_dim, n_heads_total, seq_len, delta,
+                                                ctypes.byref(g), ctypes.byref(a)))
+    return g.value, a.value
+
+
+def spectral_overflow_terms(d_model: int, head_dim: int, seq_len: int, alpha: float,
+                            gamma: float) -> tuple[float, float]:
+    t1, t2 = ctypes.c_double(), ctypes.c_double()
+    _check(load_library().spectral_overflow_terms(d_model, head_dim, seq_len, alpha, gamma,
+                                                  ctypes.byref(t1), ctypes.byref(t2)))
+    return t1.value, t2.value
+
+
+def spectral_auto_alpha(slack: Sequence[float], quantile: float = 0.9999, kappa: float = 1.0) -> float:
+    arr = (ctypes.c_double * len(slack))(*slack)
+    out = ctypes.c_double()
+    _check(load_library().spectral_auto_alpha(arr, len(slack), quantile, kappa, ctypes.byref(out)))
+    return out.value
+
+
+def spectral_slack_ratio(max_abs_logit: float, sigma_layer: float, d_model: int, head_dim: int) -> float:
+    return load_library().spectral_slack_ratio(max_abs_logit, sigma_layer, d_model, head_dim)
 
 
 # ----------------------------------------------------------- torch wrapper

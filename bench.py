@@ -5,12 +5,14 @@ power-iteration steps each (one W_K sweep from v, then per step one fused W_Q
 sweep and one fused W_K sweep), plus the per-layer E4M3 scale.  Weights,
 start vectors and outputs are resident in HBM before the timed region.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload KEY]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload KEY] [--form chain|gram]
 
 Prints one JSON line.  ``value`` is heads*iterations per second over all
-layers; ``roofline`` reports the W_Q sweep kernel (the dominant one) against
-the HBM peak; ``cpu_baseline`` times the float64 oracle on host cores over a
-bounded sample of the same workload.
+layers; ``roofline`` reports the dominant kernel against the HBM peak (the
+W_Q sweep of the default sweep chain; the Gram sweep with ``--form gram``,
+which runs the same iterates through d_h x d_h Gram matrices);
+``cpu_baseline`` times the float64 oracle on host cores over a bounded sample
+of the same workload.
 """
 
 from __future__ import annotations
@@ -43,6 +45,8 @@ def parse():
     p.add_argument("--q-strips", type=int, default=0, help="column strips per head in the W_Q sweep (0 = auto)")
     p.add_argument("--k-strips", type=int, default=0, help="column strips per KV head in the W_K sweep (0 = auto)")
     p.add_argument("--flags", type=int, default=0, help="sn_params.flags (SN_FLAG_* bits)")
+    p.add_argument("--form", choices=("chain", "gram"), default="chain",
+                   help="gram: the Gram form of the iteration (adds SN_FLAG_GRAM)")
     p.add_argument("--mode", choices=("bench", "copy"), default="bench",
                    help="copy: one plain device copy of --copy-bytes, the reference for HBM byte counters")
     p.add_argument("--copy-bytes", type=int, default=4 << 30)
@@ -123,6 +127,7 @@ def main():
     import torch
 
     from paper_2602_18851_amd import Spectral
+    from paper_2602_18851_amd.spectral import SN_FLAG_GRAM
     from workloads import WORKLOADS, all_weights, start_vectors
 
     wl = WORKLOADS[args.workload]
@@ -135,8 +140,10 @@ def main():
     sigma = torch.empty(wl.n_layers, wl.n_q, dtype=torch.float32, device=dev)
     scale = torch.empty(wl.n_layers, dtype=torch.float32, device=dev)
     iters = torch.empty(wl.n_layers, wl.n_q, dtype=torch.int32, device=dev)
+    gram = args.form == "gram"
+    flags = args.flags | (SN_FLAG_GRAM if gram else 0)
     est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=0.0,
-                   q_strips=args.q_strips, k_strips=args.k_strips, flags=args.flags)
+                   q_strips=args.q_strips, k_strips=args.k_strips, flags=flags)
     torch.cuda.synchronize()
 
     def step():
@@ -162,18 +169,26 @@ def main():
     step()
     prof = est.profile_read()
     est.profile(False)
-    q_ms, q_n = prof["q_sweep"]
-    k_ms, k_n = prof["k_sweep"]
-    i_ms, _ = prof["k_sweep_first"]
-    f_ms, _ = prof["finalize"]
-
-    e = wl.elem_bytes
     H = wl.n_layers * wl.n_q
     q_bytes, k_bytes = wl.weight_bytes()
-    q_alg = q_bytes + H * 2 * wl.head_dim * 4          # weights + z in + y out, per launch
-    q_avg_ms = q_ms / q_n
-    achieved = q_alg / (q_avg_ms * 1e-3) / 1e9
-    call_bytes = n_iter * (q_bytes + k_bytes) + k_bytes + 12 * wl.d_model * H
+    if gram:
+        # Gram sweep: every weight read once, the upper-triangle 16 x 16 Gram
+        # blocks written once per query / key head (d_h (d_h + 16) / 2 floats)
+        units = H + wl.n_layers * wl.n_kv
+        g_out = units * wl.head_dim * (wl.head_dim + 16) // 2 * 4
+        dom_name, dom_kind = "gram_sweep (G = R R^T of every head, matrix cores)", "gram_sweep"
+        dom_alg = q_bytes + k_bytes + g_out
+        dom_flops = 2.0 * units * wl.head_dim * (wl.head_dim + 16) / 2 * wl.d_model
+        # first W_K sweep, Gram sweep, final W_K sweep, Gram blocks read back, vectors
+        call_bytes = 3 * k_bytes + q_bytes + 2 * g_out + 12 * wl.d_model * H
+    else:
+        dom_name, dom_kind = "q_sweep (fused W_Q sweep)", "q_sweep"
+        dom_alg = q_bytes + H * 2 * wl.head_dim * 4          # weights + z in + y out, per launch
+        dom_flops = None
+        call_bytes = n_iter * (q_bytes + k_bytes) + k_bytes + 12 * wl.d_model * H
+    dom_ms, dom_n = prof[dom_kind]
+    dom_avg_ms = dom_ms / dom_n
+    achieved = dom_alg / (dom_avg_ms * 1e-3) / 1e9
     heads_iters = H * n_iter
     out = {
         "metric": METRIC,
@@ -194,25 +209,30 @@ def main():
             "n_layers": wl.n_layers, "d_model": wl.d_model, "n_q_heads": wl.n_q, "n_kv_heads": wl.n_kv,
             "head_dim": wl.head_dim, "weights_dtype": wl.dtype, "n_iter": n_iter, "heads": H,
             "start": "cold (seeded unit vectors), state carried across steps",
+            "form": args.form,
         },
         "effective_GBps": call_bytes / (ms * 1e-3) / 1e9,
         "effective_frac_of_peak": call_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "call_bytes": call_bytes,
         "wall_s_timed": wall_s,
-        "kernels_ms_per_step": {"k_sweep_first": i_ms, "q_sweep": q_ms, "k_sweep": k_ms, "finalize": f_ms},
+        "kernels_ms_per_step": {k: t for k, (t, n) in prof.items() if n},
         "roofline": {
-            "kernel": "q_sweep (fused W_Q sweep)",
+            "kernel": dom_name,
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": measured_traffic(q_alg),
-            "algorithmic_bytes_per_launch": q_alg,
-            "avg_launch_ms": q_avg_ms,
-            "launches": q_n,
+            "traffic": None if gram else measured_traffic(dom_alg),
+            "algorithmic_bytes_per_launch": dom_alg,
+            "avg_launch_ms": dom_avg_ms,
+            "launches": dom_n,
         },
     }
+    if dom_flops:
+        out["roofline"]["mfma_TFLOPs"] = dom_flops / (dom_avg_ms * 1e-3) / 1e12
+        out["roofline"]["mfma_frac_of_dense_peak"] = out["roofline"]["mfma_TFLOPs"] / (2500.0 if wl.dtype == "bf16"
+                                                                                        else 157.3)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, n_iter)
     print(json.dumps(out), flush=True)

@@ -63,7 +63,8 @@ typedef struct {
   int32_t d_model;     /* d >= 1: model width (LayerNorm/RMSNorm width, Sec. 3.1) */
   int32_t n_q_heads;   /* n_q >= 1                                                */
   int32_t n_kv_heads;  /* n_kv >= 1, divides n_q (n_kv == n_q: multi-head)        */
-  int32_t head_dim;    /* d_h: one of 8, 16, 32, 64, 128                          */
+  int32_t head_dim;    /* d_h: one of 8, 16, 32, 64, 128; d_h * ld * element size
+                          must stay below 2^31 bytes                              */
   int32_t dtype;       /* sn_dtype of the weights; vectors are always float32     */
   int64_t ld;          /* row stride of wq and wk in elements; 0 means d_model.
                           ld * element size must be a multiple of 16 bytes.       */
@@ -85,6 +86,20 @@ typedef struct {
  * matrix-core kernel applies (bf16 weights, d_h 64 or 128, >= 3 query heads
  * per KV head).  Results agree to rounding; the flag exists for comparison. */
 #define SN_FLAG_VALU_K_SWEEP 1
+
+/* Gram form of the same iteration.  For one head, ||W^Q z||^2 = z^T G_Q z
+ * with G_Q = Q_h Q_h^T (d_h x d_h), and ||W^K y||^2 = y^T G_K y with
+ * G_K = K_j K_j^T, so the step maps of Sec. 4.1 factor through the two Gram
+ * matrices:  y = G_Q z / sigma,  z_next = G_K y / ||v'||.  With this flag one
+ * sweep over all weights forms G_Q for every query head and G_K for every
+ * key head on the matrix cores, the iteration runs in d_h-space, and one
+ * final W_K sweep (plus one W_Q sweep when u is requested) maps the last y
+ * (z) back to v (u).  The iterates, sigma, u and v are those of the default
+ * path up to rounding; the weights are read about four times per call
+ * instead of twice per iteration.  Needs head_dim >= 16.  The workspace
+ * grows by the Gram partials, 2 d_h (d_h + 16) bytes per query or key head
+ * and column strip (spectral_workspace_bytes gives the total). */
+#define SN_FLAG_GRAM 2
 
 
 typedef struct sn_ctx sn_ctx;
@@ -117,7 +132,7 @@ SN_API int spectral_init(sn_ctx** ctx, const sn_shape* shape, const sn_params* p
  *              start vector, u = 0).
  * The call is queued asynchronously on the context's stream.  With tol > 0
  * it waits on the stream at iterations 2, 3, 4, 6, 9, ... to stop queueing
- * once every head has converged.  Weights and vectors must not alias the
+ * once every head has converged (not in the Gram form, which never waits).  Weights and vectors must not alias the
  * outputs.  Errors: SN_ENULL, SN_EINVAL, SN_EHIP. */
 SN_API int spectral_step(sn_ctx* ctx, const void* const* wq_layers, const void* const* wk_layers,
                          float* v, float* u, int32_t n_iter, float* sigma, float* scale,
@@ -139,9 +154,12 @@ SN_API int spectral_workspace_bytes(const sn_shape* shape, const sn_params* para
 /* Per-kernel timing.  With enable != 0 every later launch is bracketed by
  * HIP events on the context's stream.  spectral_profile_read waits for the
  * stream and returns, per kernel kind (0 = first W_K sweep from v,
- * 1 = W_Q sweep, 2 = W_K sweep, 3 = finalize), the summed device time in
+ * 1 = W_Q sweep, 2 = W_K sweep, 3 = finalize, 4 = Gram sweep, 5 = d_h-space
+ * iteration, 6 = final sweeps of the Gram form), the summed device time in
  * milliseconds and the number of launches since the previous read, then
- * resets both.  ms and launches point to 4 host elements each. */
+ * resets both.  ms and launches point to SN_PROFILE_KINDS host elements
+ * each. */
+#define SN_PROFILE_KINDS 7
 SN_API int spectral_profile(sn_ctx* ctx, int32_t enable);
 SN_API int spectral_profile_read(sn_ctx* ctx, double* ms, int64_t* launches);
 

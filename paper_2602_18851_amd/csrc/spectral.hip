@@ -70,8 +70,12 @@ constexpr int kKMfmaResident = 3072;  // waves of the matrix-core W_K sweep resi
 constexpr int kRsrcWord3 = 0x00020000; // buffer descriptor word 3 for gfx9-family raw loads
 constexpr int kStreamPolicy = 2;       // cache policy of the weight loads: non-temporal (read once per sweep)
 
-enum { PH_INIT = 0, PH_Q = 1, PH_K = 2 };
-enum { KIND_INIT = 0, KIND_Q = 1, KIND_K = 2, KIND_FIN = 3, KIND_N = 4 };
+// Sweep phases: the first W_K sweep from v, the W_Q and W_K sweeps of a step,
+// and the two final sweeps of the Gram form (v' = K_j^T y and u' = Q_h^T z
+// from the d_h-vectors the Gram iteration leaves behind).
+enum { PH_INIT = 0, PH_Q = 1, PH_K = 2, PH_EK = 3, PH_EQ = 4 };
+enum { KIND_INIT = 0, KIND_Q = 1, KIND_K = 2, KIND_FIN = 3, KIND_GRAM = 4, KIND_ITER = 5, KIND_EMIT = 6, KIND_N = 7 };
+static_assert(KIND_N == SN_PROFILE_KINDS, "profile kinds");
 
 struct Work {
   float* zp;         // [2][H][Sk][DH]  W_K-sweep partials of z, by step parity
@@ -83,6 +87,7 @@ struct Work {
   int32_t* alive;    // [2][H]          head continues after the step of that parity
   int32_t* n_alive;  // [2]             heads still running after a W_K sweep
   int32_t* iters;    // [H]             used when the caller passes no iters array
+  float* fin;        // [H][2][DH]      Gram form: z and y of each head's last step
 };
 
 struct SweepArgs {
@@ -102,6 +107,7 @@ struct SweepArgs {
 
 struct FinArgs {
   int32_t H, L, n_q, d, s_k;
+  int32_t slot_fixed;  // workspace slot of the ||v'||^2 partials; -1: parity of the last step
   float coef;
   Work w;
   float* v;
@@ -187,7 +193,7 @@ __device__ __forceinline__ Item decode_item(const SweepArgs& a, int item) {
   const bool valid_item = item < a.n_items;
   it.strip = valid_item ? item % a.s_out : 0;
   const int rest = valid_item ? item / a.s_out : 0;
-  if (PH == PH_Q) {
+  if (PH == PH_Q || PH == PH_EQ) {  // one query head per item
     it.layer = rest / a.n_q;
     it.row0 = (rest % a.n_q) * DH;
     it.head0 = rest;
@@ -228,6 +234,15 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
     if (PH == PH_INIT) {
       act[i] = true;
       if (strip == 0 && lane == 0) a.w.alive[hh] = 1;  // slot 0
+      continue;
+    }
+    if (PH == PH_EK || PH == PH_EQ) {  // final sweeps of the Gram form: heads that ran
+      act[i] = uni(a.iters[hh]) > 0;
+      last[i] = act[i];
+      if (act[i]) {
+        const float* src = a.w.fin + (size_t)hh * 2 * DH + (PH == PH_EK ? DH : 0);
+        for (int r = lane; r < DH; r += 64) xs[i][r] = src[r];
+      }
       continue;
     }
     bool alive = uni(a.w.alive[slot_prev * a.H + hh]) != 0;
@@ -423,14 +438,16 @@ sweep_kernel(SweepArgs a) {
       for (int c = 0; c < VEC; ++c) nrm[i] = fmaf(w[c], w[c], nrm[i]);
 
       // full d-space vector of the final step: v' (W_K sweep) or u' (W_Q sweep)
-      const bool write_vec = (PH == PH_K) ? last[i] : (PH == PH_Q && a.want_vec);
+      constexpr bool V_OUT = PH == PH_K || PH == PH_EK;
+      const bool write_vec = V_OUT ? last[i] : (PH == PH_EQ || (PH == PH_Q && a.want_vec));
       if (write_vec && rg == 0) {
-        float* out = ((PH == PH_K) ? a.v : a.u) + (size_t)hh * a.d + col;
+        float* out = (V_OUT ? a.v : a.u) + (size_t)hh * a.d + col;
 #pragma unroll
         for (int c = 0; c < VEC; ++c)
           if (FULL || c < nval) out[c] = w[c];
       }
-      if (PH == PH_K && last[i]) continue;  // z of a finished head is not needed
+      // z of a finished head is not needed; the final sweeps produce no z or y
+      if ((PH == PH_K && last[i]) || PH == PH_EK || PH == PH_EQ) continue;
 #pragma unroll
       for (int rr = 0; rr < RPL; ++rr) {
         float s = acc[i][rr];
@@ -453,6 +470,7 @@ sweep_kernel(SweepArgs a) {
     tile_step(std::false_type{}, n_full, cur);
   }
 
+  if (PH == PH_EQ) return;  // u' is the only output
   // ---- reduce over the 8 column chunks and write this strip's partials
   float* outp = (PH == PH_Q) ? a.w.yp : a.w.zp + (size_t)slot_cur * a.H * a.s_k * DH;
   float* outn = (PH == PH_Q) ? a.w.yn : a.w.zn + (size_t)slot_cur * a.H * a.s_k;
@@ -464,7 +482,7 @@ sweep_kernel(SweepArgs a) {
 #pragma unroll
     for (int m = 1; m < CPL; m <<= 1) n = xor_sum(n, m);
     if (lane == 0) outn[(size_t)hh * a.s_out + strip] = n;
-    if (PH == PH_K && last[i]) continue;
+    if ((PH == PH_K && last[i]) || PH == PH_EK) continue;
     float* op = outp + ((size_t)hh * a.s_out + strip) * DH + rg * RPL;
 #pragma unroll
     for (int rr = 0; rr < RPL; ++rr) {
@@ -557,8 +575,10 @@ ksweep_mfma_kernel(SweepArgs a) {
   const bool act_s = pick(act, s >> 1), last_s = pick(last, s >> 1);
   const bool lo_part = (s & 1) != 0;
 
+  constexpr bool PROD1 = PH == PH_K || PH == PH_EK;  // v' = K^T y
+  constexpr bool PROD2 = PH != PH_EK;                // z = K v'
   bf16x8 a1[KB];  // Y^T fragments: slot s, rows 32 kb + 8 g + t
-  if (PH == PH_K) {
+  if (PROD1) {
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
@@ -615,7 +635,7 @@ ksweep_mfma_kernel(SweepArgs a) {
     }
 
     bf16x8 b2[KC];
-    if (PH == PH_K) {
+    if (PROD1) {
       f32x4 d1[CB];
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb) d1[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -647,6 +667,7 @@ ksweep_mfma_kernel(SweepArgs a) {
           if (last0) a.v[(size_t)(head0 + 2 * g) * a.d + col] = v0;
           if (last1) a.v[(size_t)(head0 + 2 * g + 1) * a.d + col] = v1;
         }
+        if (!PROD2) continue;
         const __bf16 h0 = (__bf16)v0, h1 = (__bf16)v1;
         const __bf16 l0 = (__bf16)(v0 - (float)h0), l1 = (__bf16)(v1 - (float)h1);
         const int c = 16 * cb + s;
@@ -655,9 +676,11 @@ ksweep_mfma_kernel(SweepArgs a) {
         vl[(4 * g + 2) * kMVPitch + c] = __builtin_bit_cast(uint16_t, h1);
         vl[(4 * g + 3) * kMVPitch + c] = __builtin_bit_cast(uint16_t, l1);
       }
+      if (PROD2) {
 #pragma unroll
-      for (int kc = 0; kc < KC; ++kc)
-        b2[kc] = *reinterpret_cast<const bf16x8*>(vl + s * kMVPitch + 32 * kc + 8 * g);
+        for (int kc = 0; kc < KC; ++kc)
+          b2[kc] = *reinterpret_cast<const bf16x8*>(vl + s * kMVPitch + 32 * kc + 8 * g);
+      }
     } else {  // first sweep: v' is the start vector itself
       const float* vrow = a.v + (size_t)(head0 + (s >> 1)) * a.d;
 #pragma unroll
@@ -672,12 +695,14 @@ ksweep_mfma_kernel(SweepArgs a) {
         }
     }
 
+    if (PROD2) {
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
+      for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int kc = 0; kc < KC; ++kc)
-        zacc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, cur[rb][kc]), b2[kc],
-                                                           zacc[rb], 0, 0, 0);
+        for (int kc = 0; kc < KC; ++kc)
+          zacc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, cur[rb][kc]), b2[kc],
+                                                             zacc[rb], 0, 0, 0);
+    }
   }
 
   // ---- partials of this strip
@@ -688,12 +713,12 @@ ksweep_mfma_kernel(SweepArgs a) {
   for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
     for (int j = 0; j < 4; ++j) zacc[rb][j] += __shfl_xor(zacc[rb][j], 1);
-  if (!lo_part && act_s && !last_s) {
+  if (PROD2 && !lo_part && act_s && !last_s) {
     float* op = zp_out + ((size_t)(head0 + (s >> 1)) * a.s_out + strip) * DH + 4 * g;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) *reinterpret_cast<f32x4*>(op + 16 * rb) = zacc[rb];
   }
-  if (PH == PH_K) {  // lane (g, s) summed columns of heads 2g, 2g+1: reduce over s
+  if (PROD1) {  // lane (g, s) summed columns of heads 2g, 2g+1: reduce over s
 #pragma unroll
     for (int m = 1; m < 16; m <<= 1) {
       nrm0 += __shfl_xor(nrm0, m);
@@ -710,6 +735,330 @@ ksweep_mfma_kernel(SweepArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Gram form (SN_FLAG_GRAM).  With G_Q = Q_h Q_h^T and G_K = K_j K_j^T
+// (d_h x d_h), one step of the iteration is
+//     w = G_Q z,  sigma^2 = z^T w,  y = w / sigma,
+//     t = G_K y,  ||v'||^2 = y^T t,  z_next = t / ||v'||,
+// because u' = Q_h^T z has ||u'||^2 = z^T G_Q z and Q_h u' = G_Q z, and
+// likewise for v' = K_j^T y.  These are the iterates of the sweeps above,
+// computed in d_h-space.
+//
+// gram_kernel forms G = R R^T for every d_h x d row block R (query heads
+// first, then key heads) on the matrix cores: an output block (bi, bj) of
+// 16 x 16 is one MFMA chain whose A operand is rows 16 bi.. of R and whose B
+// operand is rows 16 bj.. of R, both in the rows' native layout (lane l
+// holds row l % 16 and 16 bytes of consecutive columns; the contraction
+// index may be permuted freely as long as both operands share it).  Only the
+// upper triangle of blocks is formed.  Two loads per 16-row block cover one
+// 128-byte segment of each row, back to back.
+constexpr int kGWaves = 4;                 // waves per workgroup of the Gram sweep
+constexpr int kGTargetItems = 4096;        // Gram work items aimed for (about two waves per SIMD)
+
+struct GramArgs {
+  const void* const* mats;  // device table: wq pointers of all layers, then wk pointers
+  int64_t ld;
+  int32_t d, L, n_q, n_kv, H;
+  int32_t s_g, tps, n_tiles, n_items;
+  float* gp;  // [units][s_g][NB][64 lanes][4]: partial Gram blocks in the MFMA output layout
+};
+
+template <int RB>
+__host__ __device__ constexpr int tri_index(int bi, int bj) {  // bj >= bi
+  return bi * RB - bi * (bi - 1) / 2 + (bj - bi);
+}
+
+template <typename T, int DH>
+__global__ void __launch_bounds__(64 * kGWaves) __attribute__((amdgpu_waves_per_eu(DH >= 128 ? 2 : 4)))
+gram_kernel(GramArgs a) {
+  constexpr int ES = sizeof(T);
+  constexpr int RB = DH / 16;
+  constexpr int NB = RB * (RB + 1) / 2;
+  constexpr int TC = 128 / ES;  // columns per tile
+  const int lane = threadIdx.x & 63;
+  const int wv = uni((int)(threadIdx.x >> 6));
+  const int q = lane >> 4, s = lane & 15;
+  const int item = blockIdx.x * kGWaves + wv;
+  if (item >= a.n_items) return;
+  const int unit = item / a.s_g, strip = item % a.s_g;
+  int layer, row0, tab;
+  if (unit < a.H) {
+    layer = unit / a.n_q;
+    row0 = (unit % a.n_q) * DH;
+    tab = layer;
+  } else {
+    layer = (unit - a.H) / a.n_kv;
+    row0 = ((unit - a.H) % a.n_kv) * DH;
+    tab = a.L + layer;
+  }
+  const char* blk = uni(a.mats[tab]) + (int64_t)row0 * a.ld * ES;
+  const uint32_t nrec = (uint32_t)((((int64_t)(DH - 1) * a.ld + a.d) * ES + 15) & ~int64_t(15));
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(blk), (short)0, (int)nrec, kRsrcWord3);
+  const uint32_t lane_off = (uint32_t)((int64_t)s * a.ld * ES + 16 * q);
+  const uint32_t row_bytes = (uint32_t)(a.ld * ES);
+
+  f32x4 acc[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int n_full = a.d / TC;
+  const int t0 = strip * a.tps;
+  const int t1 = min(t0 + a.tps, a.n_tiles);
+
+#pragma unroll 1
+  for (int t = t0; t < t1; ++t) {
+    u32x4 fr[RB][2];
+    const uint32_t voff = lane_off + (uint32_t)(t * 128);
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int kc = 0; kc < 2; ++kc)
+        fr[rb][kc] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff + 64 * kc, 16 * rb * row_bytes, kStreamPolicy);
+    if (t >= n_full) {  // the ragged last tile: zero columns >= d
+#pragma unroll
+      for (int kc = 0; kc < 2; ++kc) {
+        const int nval = a.d - (t * TC + (64 * kc + 16 * q) / ES);
+        u32x4 m;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (ES == 2)
+            m[e] = (2 * e < nval ? 0x0000ffffu : 0u) | (2 * e + 1 < nval ? 0xffff0000u : 0u);
+          else
+            m[e] = e < nval ? 0xffffffffu : 0u;
+        }
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) fr[rb][kc] &= m;
+      }
+    }
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc)
+#pragma unroll
+      for (int bi = 0; bi < RB; ++bi)
+#pragma unroll
+        for (int bj = bi; bj < RB; ++bj) {
+          f32x4& c = acc[tri_index<RB>(bi, bj)];
+          if constexpr (ES == 2) {
+            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, fr[bi][kc]),
+                                                        __builtin_bit_cast(bf16x8, fr[bj][kc]), c, 0, 0, 0);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(fr[bi][kc][e]),
+                                                       __uint_as_float(fr[bj][kc][e]), c, 0, 0, 0);
+          }
+        }
+  }
+  f32x4* out = reinterpret_cast<f32x4*>(a.gp) + ((size_t)item * NB) * 64 + lane;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) out[(size_t)b * 64] = acc[b];
+}
+
+// d_h-space iteration of the Gram form: one workgroup of NT threads per query
+// head.  Thread t = 16 R + C owns rows RPT R .. RPT R + RPT - 1 and columns
+// CPT C .. CPT C + CPT - 1 (CPT = d_h / 16) of G_Q and of G_K in registers.
+// A product G x reads CPT entries of x from LDS and sums the partial rows
+// over the 16 lanes C = 0..15 of a DPP row with a butterfly (quad xor 1,
+// xor 2, half-row mirror, row mirror) that leaves the same bits in every
+// lane.  Norms are summed in a fixed order, and every thread takes the same
+// per-head decisions from the same values.
+struct IterArgs {
+  int32_t H, n_q, n_kv, g, s_k, s_g, n_iter;
+  float tol;
+  const float* gp;
+  Work w;
+  float* sigma;
+  int32_t* iters;
+};
+
+template <int DH>
+struct IterShape {
+  static constexpr int RPT = DH >= 32 ? DH / 32 : 1;  // rows per thread
+  static constexpr int CPT = DH / 16;                 // columns per thread
+  static constexpr int NT = 16 * DH / RPT;            // threads per workgroup
+  static constexpr int NW = NT / 64;                  // waves per workgroup
+  static constexpr int RB = DH / 16, NB = RB * (RB + 1) / 2;
+};
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_add(float x) {
+  return x + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the 16 lanes of a DPP row; every lane of the row gets the same bits.
+__device__ __forceinline__ float row16_sum(float x) {
+  x = dpp_add<0xB1>(x);   // quad_perm [1, 0, 3, 2]
+  x = dpp_add<0x4E>(x);   // quad_perm [2, 3, 0, 1]
+  x = dpp_add<0x141>(x);  // row_half_mirror: quad 0 <-> 1, 2 <-> 3
+  x = dpp_add<0x140>(x);  // row_mirror: half 0 <-> half 1
+  return x;
+}
+
+// Sum of the values of lanes 0, 16, 32, 48 (the C == 0 lanes), in that order.
+__device__ __forceinline__ float c0_lanes_sum(float x) {
+  const int b = __builtin_bit_cast(int, x);
+  return (__builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 0)) +
+          __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 16))) +
+         (__builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 32)) +
+          __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 48)));
+}
+
+template <int NW>
+__device__ __forceinline__ float sum_waves(const float* red) {
+  float s = 0.f;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) s += red[w];
+  return s;
+}
+
+// Sums the strips of one Gram matrix (upper-triangle 16 x 16 blocks in the
+// MFMA output layout), writes the whole symmetric matrix to LDS and hands
+// each thread its RPT x CPT sub-block.
+template <int DH>
+__device__ __forceinline__ void gram_to_regs(const float* src, int s_g, float* gl,
+                                             float (&reg)[IterShape<DH>::RPT][IterShape<DH>::CPT]) {
+  using S = IterShape<DH>;
+  constexpr int P = DH + 1, NE = S::NB * 256, NL = (NE + S::NT - 1) / S::NT;
+  const int t = threadIdx.x;
+  float x[NL];  // flat elements t, t + NT, ... of the blocks, summed over the strips
+#pragma unroll
+  for (int m = 0; m < NL; ++m) x[m] = (m * S::NT + t < NE) ? src[m * S::NT + t] : 0.f;
+  for (int st = 1; st < s_g; ++st) {
+#pragma unroll
+    for (int m = 0; m < NL; ++m)
+      if (m * S::NT + t < NE) x[m] += src[(size_t)st * NE + m * S::NT + t];
+  }
+#pragma unroll
+  for (int m = 0; m < NL; ++m) {
+    const int f = m * S::NT + t;
+    if (f >= NE) continue;
+    const int b = f >> 8, ln = (f & 255) >> 2, e = f & 3;  // block, lane and element in the MFMA layout
+    int bi = 0, start = 0;
+    while (b >= start + (S::RB - bi)) {  // upper-triangle block b -> (bi, bj)
+      start += S::RB - bi;
+      ++bi;
+    }
+    const int bj = bi + (b - start);
+    const int r = 16 * bi + 4 * (ln >> 4) + e, c = 16 * bj + (ln & 15);
+    gl[r * P + c] = x[m];
+    if (bi != bj) gl[c * P + r] = x[m];
+  }
+  __syncthreads();
+  const int R = t >> 4, C = t & 15;
+#pragma unroll
+  for (int i = 0; i < S::RPT; ++i)
+#pragma unroll
+    for (int j = 0; j < S::CPT; ++j) reg[i][j] = gl[(S::RPT * R + i) * P + S::CPT * C + j];
+  __syncthreads();
+}
+
+// out[i] = sum_c G[RPT R + i][c] x[c], complete in every lane of the row.
+template <int RPT, int CPT>
+__device__ __forceinline__ void gram_matvec(const float (&g)[RPT][CPT], const float* x, int C, float (&out)[RPT]) {
+  float xv[CPT];
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) xv[j] = x[CPT * C + j];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    float acc = 0.f;
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) acc = fmaf(g[i][j], xv[j], acc);
+    out[i] = row16_sum(acc);
+  }
+}
+
+template <int DH>
+__global__ void __launch_bounds__(IterShape<DH>::NT) gram_iterate_kernel(IterArgs a) {
+  using S = IterShape<DH>;
+  constexpr int RPT = S::RPT, CPT = S::CPT, NW = S::NW;
+  __shared__ float gl[DH * (DH + 1)];
+  __shared__ float wb[DH], tb[DH];
+  __shared__ float red_a[NW], red_b[NW];
+  const int h = blockIdx.x, t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  const int R = t >> 4, C = t & 15;
+  const int layer = h / a.n_q;
+  const int j = layer * a.n_kv + (h % a.n_q) / a.g;
+
+  // start vector: ||v||^2 and z = K_j v from the first W_K sweep (slot 0)
+  float nv2 = 0.f;
+  for (int st = 0; st < a.s_k; ++st) nv2 += a.w.zn[(size_t)h * a.s_k + st];
+  if (t == 0) a.w.vnorm0[h] = sqrtf(nv2);
+  if (!(nv2 > 0.f) || !isfinite(nv2)) {
+    if (t == 0) {
+      a.sigma[h] = __builtin_nanf("");
+      a.iters[h] = -1;
+    }
+    return;
+  }
+  const float inv0 = 1.0f / sqrtf(nv2);
+  if (t < DH) {
+    float z = 0.f;
+    for (int st = 0; st < a.s_k; ++st) z += a.w.zp[((size_t)h * a.s_k + st) * DH + t];
+    tb[t] = z * inv0;
+  }
+  float gq[RPT][CPT], gk[RPT][CPT];
+  gram_to_regs<DH>(a.gp + (size_t)h * a.s_g * S::NB * 256, a.s_g, gl, gq);
+  gram_to_regs<DH>(a.gp + (size_t)(a.H + j) * a.s_g * S::NB * 256, a.s_g, gl, gk);
+
+  float zscale = 1.f, prev = 0.f;
+  float out[RPT];
+#pragma unroll 1
+  for (int k = 1;; ++k) {
+    // w = G_Q z with z = zscale * tb; lane C == 0 of row band R owns rows RPT R ..
+    gram_matvec<RPT, CPT>(gq, tb, C, out);
+    float part = 0.f;
+    if (C == 0) {
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) {
+        const float wr = out[i] * zscale;
+        part = fmaf(tb[RPT * R + i] * zscale, wr, part);
+        wb[RPT * R + i] = wr;
+      }
+    }
+    part = c0_lanes_sum(part);
+    if (lane == 0) red_a[wv] = part;
+    __syncthreads();
+    const float s2 = sum_waves<NW>(red_a);
+    const float sig = sqrtf(s2);
+    if (s2 == 0.f) {  // M v = 0
+      if (t == 0) {
+        a.sigma[h] = 0.f;
+        a.iters[h] = -2;
+      }
+      return;
+    }
+    const bool last = (k >= a.n_iter) || (a.tol > 0.f && k >= 2 && fabsf(sig - prev) <= a.tol * sig);
+    const float inv = 1.0f / sig;
+    if (last) {
+      if (t < DH) {
+        a.w.fin[(size_t)h * 2 * DH + t] = tb[t] * zscale;     // z of the last step
+        a.w.fin[(size_t)h * 2 * DH + DH + t] = wb[t] * inv;   // y = Q_h u
+      }
+      if (t == 0) {
+        a.sigma[h] = sig;
+        a.iters[h] = k;
+      }
+      return;
+    }
+    // t = G_K y with y = w / sigma
+    gram_matvec<RPT, CPT>(gk, wb, C, out);
+    float part2 = 0.f;
+    if (C == 0) {
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) {
+        const float tr = out[i] * inv;
+        part2 = fmaf(wb[RPT * R + i] * inv, tr, part2);
+        tb[RPT * R + i] = tr;
+      }
+    }
+    part2 = c0_lanes_sum(part2);
+    if (lane == 0) red_b[wv] = part2;
+    __syncthreads();
+    const float n2 = sum_waves<NW>(red_b);
+    zscale = 1.0f / sqrtf(n2);
+    prev = sig;
+  }
+}
+
 // Normalises the final vectors and computes the per-layer scale.
 // Blocks [0, H): one head each; blocks [H, H + L): one layer each.
 __global__ void __launch_bounds__(kThreads) finalize_kernel(FinArgs f) {
@@ -720,7 +1069,8 @@ __global__ void __launch_bounds__(kThreads) finalize_kernel(FinArgs f) {
     bool touch_v = false;
     if (it > 0) {
       float n2 = 0.f;
-      for (int s = 0; s < f.s_k; ++s) n2 += f.w.zn[((size_t)(it & 1) * f.H + b) * f.s_k + s];
+      const int slot = f.slot_fixed >= 0 ? f.slot_fixed : (it & 1);
+      for (int s = 0; s < f.s_k; ++s) n2 += f.w.zn[((size_t)slot * f.H + b) * f.s_k + s];
       vs = 1.0f / sqrtf(n2);
       us = 1.0f / f.sigma[b];
       touch_v = true;
@@ -763,7 +1113,9 @@ struct Plan {
   int tile_cq, n_tiles_q;                    // W_Q sweep
   bool mfma_k;  // W_K sweeps on the matrix cores
   int s_q, tps_q, s_k, tps_k;
-  size_t off_zp, off_zn, off_yp, off_yn, off_sig, off_vn, off_alive, off_nalive, off_iters, bytes;
+  bool gram;    // Gram form
+  int units_g, s_g, tps_g, n_tiles_g, nb_g;
+  size_t off_zp, off_zn, off_yp, off_yn, off_sig, off_vn, off_alive, off_nalive, off_iters, off_fin, off_gp, bytes;
 };
 
 int esize(int dtype) { return dtype == SN_F32 ? 4 : 2; }
@@ -788,7 +1140,10 @@ int validate(const sn_shape* s, const sn_params* p) {
     return fail(SN_EINVAL, "alpha, eta_fp8 and r_max must be finite and > 0");
   if (!(p->tol >= 0.f) || !std::isfinite(p->tol)) return fail(SN_EINVAL, "tol must be finite and >= 0");
   if (p->q_strips < 0 || p->k_strips < 0) return fail(SN_EINVAL, "strip counts must be >= 0");
-  if (p->flags & ~SN_FLAG_VALU_K_SWEEP) return fail(SN_EINVAL, "unknown flag bits");
+  if (p->flags & ~(SN_FLAG_VALU_K_SWEEP | SN_FLAG_GRAM)) return fail(SN_EINVAL, "unknown flag bits");
+  if ((p->flags & SN_FLAG_GRAM) && s->head_dim < 16) return fail(SN_EINVAL, "the Gram form needs head_dim >= 16");
+  if ((int64_t)s->head_dim * ld * esize(s->dtype) >= (int64_t(1) << 31))
+    return fail(SN_EINVAL, "head_dim * ld * element size must be below 2^31 bytes");
   return SN_OK;
 }
 
@@ -825,6 +1180,14 @@ Plan make_plan(const sn_shape* s, const sn_params* p) {
   strips(pl.n_tiles_q, pl.H, p->q_strips, kQTargetItems, false, &pl.s_q, &pl.tps_q);
   strips(pl.n_tiles, (int64_t)s->n_layers * s->n_kv_heads * pl.nch, p->k_strips,
          pl.mfma_k ? kKMfmaResident : kKTargetItems, pl.mfma_k, &pl.s_k, &pl.tps_k);
+  pl.gram = (p->flags & SN_FLAG_GRAM) != 0;
+  if (pl.gram) {
+    const int rb = dh / 16;
+    pl.nb_g = rb * (rb + 1) / 2;
+    pl.units_g = pl.H + s->n_layers * s->n_kv_heads;
+    pl.n_tiles_g = ceil_div((int64_t)s->d_model * esize(s->dtype), 128);
+    strips(pl.n_tiles_g, pl.units_g, 0, kGTargetItems, true, &pl.s_g, &pl.tps_g);
+  }
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -841,6 +1204,10 @@ Plan make_plan(const sn_shape* s, const sn_params* p) {
   pl.off_alive = take(2 * H * 4);
   pl.off_nalive = take(2 * 4);
   pl.off_iters = take(H * 4);
+  if (pl.gram) {
+    pl.off_fin = take(H * 2 * dh * 4);
+    pl.off_gp = take((size_t)pl.units_g * pl.s_g * pl.nb_g * 256 * 4);
+  }
   pl.bytes = off;
   return pl;
 }
@@ -890,8 +1257,10 @@ template <typename T, int DH, int GC>
 void launch_k(int ph, dim3 grid, hipStream_t st, const SweepArgs& a) {
   if (ph == PH_INIT)
     sweep_kernel<T, DH, GC, PH_INIT><<<grid, kThreads, 0, st>>>(a);
-  else
+  else if (ph == PH_K)
     sweep_kernel<T, DH, GC, PH_K><<<grid, kThreads, 0, st>>>(a);
+  else if constexpr (DH >= 16)
+    sweep_kernel<T, DH, GC, PH_EK><<<grid, kThreads, 0, st>>>(a);
 }
 
 template <typename T, int DH>
@@ -900,13 +1269,19 @@ void launch_dh(int ph, int gc, bool mfma, dim3 grid, hipStream_t st, const Sweep
     sweep_kernel<T, DH, 1, PH_Q><<<grid, kThreads, 0, st>>>(a);
     return;
   }
+  if (ph == PH_EQ) {
+    if constexpr (DH >= 16) sweep_kernel<T, DH, 1, PH_EQ><<<grid, kThreads, 0, st>>>(a);
+    return;
+  }
   if constexpr (std::is_same<T, uint16_t>::value && (DH == 64 || DH == 128)) {
     if (mfma) {
       const dim3 mgrid(ceil_div(a.n_items, kMWaves));
       if (ph == PH_INIT)
         ksweep_mfma_kernel<DH, PH_INIT><<<mgrid, 64 * kMWaves, 0, st>>>(a);
-      else
+      else if (ph == PH_K)
         ksweep_mfma_kernel<DH, PH_K><<<mgrid, 64 * kMWaves, 0, st>>>(a);
+      else
+        ksweep_mfma_kernel<DH, PH_EK><<<mgrid, 64 * kMWaves, 0, st>>>(a);
       return;
     }
   }
@@ -929,9 +1304,28 @@ void launch_t(int dh, int ph, int gc, bool mfma, dim3 grid, hipStream_t st, cons
   }
 }
 
+// Brackets one launch with profiling events when profiling is on.
+template <typename F>
+int timed(sn_ctx* c, int kind, F&& launch) {
+  ProfRec rec{kind, nullptr, nullptr};
+  if (c->prof) {
+    rec.a = take_event(c);
+    rec.b = take_event(c);
+    if (!rec.a || !rec.b) return fail(SN_EHIP, "hipEventCreate failed");
+    SN_HIP(hipEventRecord(rec.a, c->stream));
+  }
+  launch();
+  SN_HIP(hipGetLastError());
+  if (c->prof) {
+    SN_HIP(hipEventRecord(rec.b, c->stream));
+    c->recs.push_back(rec);
+  }
+  return SN_OK;
+}
+
 int launch_sweep(sn_ctx* c, int ph, SweepArgs a) {
   const Plan& pl = c->plan;
-  if (ph == PH_Q) {
+  if (ph == PH_Q || ph == PH_EQ) {
     a.mats = c->d_tab;
     a.s_out = pl.s_q;
     a.tps = pl.tps_q;
@@ -945,22 +1339,107 @@ int launch_sweep(sn_ctx* c, int ph, SweepArgs a) {
     a.n_items = c->shape.n_layers * c->shape.n_kv_heads * pl.nch * pl.s_k;
   }
   const dim3 grid(ceil_div(a.n_items, kWaves));
-  ProfRec rec{ph == PH_INIT ? KIND_INIT : ph == PH_Q ? KIND_Q : KIND_K, nullptr, nullptr};
-  if (c->prof) {
-    rec.a = take_event(c);
-    rec.b = take_event(c);
-    if (!rec.a || !rec.b) return fail(SN_EHIP, "hipEventCreate failed");
-    SN_HIP(hipEventRecord(rec.a, c->stream));
+  const int kind = ph == PH_INIT ? KIND_INIT : ph == PH_Q ? KIND_Q : ph == PH_K ? KIND_K : KIND_EMIT;
+  return timed(c, kind, [&] {
+    if (c->shape.dtype == SN_BF16)
+      launch_t<uint16_t>(c->shape.head_dim, ph, pl.gc, pl.mfma_k, grid, c->stream, a);
+    else
+      launch_t<float>(c->shape.head_dim, ph, pl.gc, pl.mfma_k, grid, c->stream, a);
+  });
+}
+
+template <typename T>
+void gram_dispatch(int dh, dim3 grid, hipStream_t st, const GramArgs& g) {
+  switch (dh) {
+    case 16: gram_kernel<T, 16><<<grid, 64 * kGWaves, 0, st>>>(g); break;
+    case 32: gram_kernel<T, 32><<<grid, 64 * kGWaves, 0, st>>>(g); break;
+    case 64: gram_kernel<T, 64><<<grid, 64 * kGWaves, 0, st>>>(g); break;
+    default: gram_kernel<T, 128><<<grid, 64 * kGWaves, 0, st>>>(g); break;
   }
-  if (c->shape.dtype == SN_BF16)
-    launch_t<uint16_t>(c->shape.head_dim, ph, pl.gc, pl.mfma_k, grid, c->stream, a);
-  else
-    launch_t<float>(c->shape.head_dim, ph, pl.gc, pl.mfma_k, grid, c->stream, a);
-  SN_HIP(hipGetLastError());
-  if (c->prof) {
-    SN_HIP(hipEventRecord(rec.b, c->stream));
-    c->recs.push_back(rec);
+}
+
+// The sweeps of the default form: first W_K sweep, then n_iter x (W_Q sweep,
+// W_K sweep).  In tolerance mode the host polls the count of running heads at
+// iterations 2, 3, 4, 6, 9, ... and stops queueing once it is zero.
+int run_chain(sn_ctx* c, SweepArgs a, float* u) {
+  int rc;
+  a.k = 0;
+  if ((rc = launch_sweep(c, PH_INIT, a)) != SN_OK) return rc;
+  int next_check = 2;
+  for (int k = 1; k <= a.n_iter; ++k) {
+    a.k = k;
+    a.want_vec = (u != nullptr) && (c->params.tol > 0.f || k == a.n_iter);
+    if ((rc = launch_sweep(c, PH_Q, a)) != SN_OK) return rc;
+    a.want_vec = 0;
+    if ((rc = launch_sweep(c, PH_K, a)) != SN_OK) return rc;
+    if (c->params.tol > 0.f && k == next_check && k < a.n_iter) {
+      SN_HIP(hipMemcpyAsync(c->h_alive, c->w.n_alive + (k & 1), sizeof(int32_t), hipMemcpyDeviceToHost,
+                            c->stream));
+      SN_HIP(hipStreamSynchronize(c->stream));
+      if (c->h_alive[0] == 0) break;
+      next_check = k < 4 ? k + 1 : k + k / 2;
+    }
   }
+  return SN_OK;
+}
+
+// The Gram form of one call: first W_K sweep, Gram sweep, d_h-space
+// iteration, final W_K sweep (and W_Q sweep for u).
+int run_gram(sn_ctx* c, SweepArgs a, float* u) {
+  const Plan& pl = c->plan;
+  int rc;
+  a.k = 0;
+  if ((rc = launch_sweep(c, PH_INIT, a)) != SN_OK) return rc;
+
+  GramArgs g{};
+  g.mats = c->d_tab;
+  g.ld = c->shape.ld;
+  g.d = c->shape.d_model;
+  g.L = c->shape.n_layers;
+  g.n_q = c->shape.n_q_heads;
+  g.n_kv = c->shape.n_kv_heads;
+  g.H = pl.H;
+  g.s_g = pl.s_g;
+  g.tps = pl.tps_g;
+  g.n_tiles = pl.n_tiles_g;
+  g.n_items = pl.units_g * pl.s_g;
+  g.gp = reinterpret_cast<float*>(c->ws + pl.off_gp);
+  const dim3 ggrid(ceil_div(g.n_items, kGWaves));
+  const int dh = c->shape.head_dim;
+  rc = timed(c, KIND_GRAM, [&] {
+    if (c->shape.dtype == SN_BF16)
+      gram_dispatch<uint16_t>(dh, ggrid, c->stream, g);
+    else
+      gram_dispatch<float>(dh, ggrid, c->stream, g);
+  });
+  if (rc != SN_OK) return rc;
+
+  IterArgs it{};
+  it.H = pl.H;
+  it.n_q = c->shape.n_q_heads;
+  it.n_kv = c->shape.n_kv_heads;
+  it.g = pl.g;
+  it.s_k = pl.s_k;
+  it.s_g = pl.s_g;
+  it.n_iter = a.n_iter;
+  it.tol = a.tol;
+  it.gp = g.gp;
+  it.w = c->w;
+  it.sigma = a.sigma;
+  it.iters = a.iters;
+  rc = timed(c, KIND_ITER, [&] {
+    switch (dh) {
+      case 16: gram_iterate_kernel<16><<<dim3(pl.H), IterShape<16>::NT, 0, c->stream>>>(it); break;
+      case 32: gram_iterate_kernel<32><<<dim3(pl.H), IterShape<32>::NT, 0, c->stream>>>(it); break;
+      case 64: gram_iterate_kernel<64><<<dim3(pl.H), IterShape<64>::NT, 0, c->stream>>>(it); break;
+      default: gram_iterate_kernel<128><<<dim3(pl.H), IterShape<128>::NT, 0, c->stream>>>(it); break;
+    }
+  });
+  if (rc != SN_OK) return rc;
+
+  a.k = 0;  // the final sweeps write their ||v'||^2 partials to slot 0
+  if ((rc = launch_sweep(c, PH_EK, a)) != SN_OK) return rc;
+  if (u && (rc = launch_sweep(c, PH_EQ, a)) != SN_OK) return rc;
   return SN_OK;
 }
 
@@ -1014,6 +1493,7 @@ SN_API int spectral_init(sn_ctx** ctx, const sn_shape* shape, const sn_params* p
   c->w.alive = reinterpret_cast<int32_t*>(c->ws + pl.off_alive);
   c->w.n_alive = reinterpret_cast<int32_t*>(c->ws + pl.off_nalive);
   c->w.iters = reinterpret_cast<int32_t*>(c->ws + pl.off_iters);
+  c->w.fin = pl.gram ? reinterpret_cast<float*>(c->ws + pl.off_fin) : nullptr;
   *ctx = c;
   return SN_OK;
 }
@@ -1116,24 +1596,8 @@ SN_API int spectral_step(sn_ctx* c, const void* const* wq_layers, const void* co
   a.sigma = sigma;
   a.iters = iters ? iters : c->w.iters;
 
-  int rc;
-  a.k = 0;
-  if ((rc = launch_sweep(c, PH_INIT, a)) != SN_OK) return rc;
-  int next_check = 2;
-  for (int k = 1; k <= n_iter; ++k) {
-    a.k = k;
-    a.want_vec = (u != nullptr) && (c->params.tol > 0.f || k == n_iter);
-    if ((rc = launch_sweep(c, PH_Q, a)) != SN_OK) return rc;
-    a.want_vec = 0;
-    if ((rc = launch_sweep(c, PH_K, a)) != SN_OK) return rc;
-    if (c->params.tol > 0.f && k == next_check && k < n_iter) {
-      SN_HIP(hipMemcpyAsync(c->h_alive, c->w.n_alive + (k & 1), sizeof(int32_t), hipMemcpyDeviceToHost,
-                            c->stream));
-      SN_HIP(hipStreamSynchronize(c->stream));
-      if (c->h_alive[0] == 0) break;
-      next_check = k < 4 ? k + 1 : k + k / 2;
-    }
-  }
+  const int rc = pl.gram ? run_gram(c, a, u) : run_chain(c, a, u);
+  if (rc != SN_OK) return rc;
 
   FinArgs f{};
   f.H = pl.H;
@@ -1141,6 +1605,7 @@ SN_API int spectral_step(sn_ctx* c, const void* const* wq_layers, const void* co
   f.n_q = c->shape.n_q_heads;
   f.d = c->shape.d_model;
   f.s_k = pl.s_k;
+  f.slot_fixed = pl.gram ? 0 : -1;
   f.coef = (float)((double)c->params.alpha * (double)c->shape.d_model /
                    (std::sqrt((double)c->shape.head_dim) * (double)c->params.eta_fp8 * (double)c->params.r_max));
   f.w = c->w;
@@ -1149,20 +1614,7 @@ SN_API int spectral_step(sn_ctx* c, const void* const* wq_layers, const void* co
   f.sigma = sigma;
   f.scale = scale;
   f.iters = a.iters;
-  ProfRec rec{KIND_FIN, nullptr, nullptr};
-  if (c->prof) {
-    rec.a = take_event(c);
-    rec.b = take_event(c);
-    if (!rec.a || !rec.b) return fail(SN_EHIP, "hipEventCreate failed");
-    SN_HIP(hipEventRecord(rec.a, c->stream));
-  }
-  finalize_kernel<<<dim3(pl.H + L), kThreads, 0, c->stream>>>(f);
-  SN_HIP(hipGetLastError());
-  if (c->prof) {
-    SN_HIP(hipEventRecord(rec.b, c->stream));
-    c->recs.push_back(rec);
-  }
-  return SN_OK;
+  return timed(c, KIND_FIN, [&] { finalize_kernel<<<dim3(pl.H + L), kThreads, 0, c->stream>>>(f); });
 }
 
 }  // extern "C"

@@ -18,7 +18,9 @@ LIB_PATH = os.path.join(HERE, "libspectral.so")
 SN_OK, SN_EINVAL, SN_ENULL, SN_EDTYPE, SN_EHIP, SN_ESTATE = 0, -1, -2, -3, -4, -5
 SN_F32, SN_BF16 = 0, 1
 SN_FLAG_VALU_K_SWEEP = 1
-KIND_NAMES = ("k_sweep_first", "q_sweep", "k_sweep", "finalize")
+SN_FLAG_GRAM = 2
+KIND_NAMES = ("k_sweep_first", "q_sweep", "k_sweep", "finalize", "gram_sweep", "gram_iterate", "gram_final_sweeps")
+SN_PROFILE_KINDS = len(KIND_NAMES)
 
 EXPORTED = (
     "spectral_init",
@@ -156,10 +158,10 @@ def spectral_profile(ctx: int, enable: bool) -> None:
 
 
 def spectral_profile_read(ctx: int) -> dict:
-    ms = (ctypes.c_double * 4)()
-    n = (ctypes.c_int64 * 4)()
+    ms = (ctypes.c_double * SN_PROFILE_KINDS)()
+    n = (ctypes.c_int64 * SN_PROFILE_KINDS)()
     _check(load_library().spectral_profile_read(ctypes.c_void_p(ctx), ms, n))
-    return {KIND_NAMES[i]: (ms[i], n[i]) for i in range(4)}
+    return {KIND_NAMES[i]: (ms[i], n[i]) for i in range(SN_PROFILE_KINDS)}
 
 
 # ------------------------------------------------ host calibration helpers

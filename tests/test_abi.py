@@ -74,7 +74,7 @@ def test_bad_shapes_are_rejected(lib, kw, code):
 
 
 @pytest.mark.parametrize("kw", [dict(alpha=0.0), dict(eta_fp8=-1.0), dict(tol=-1e-3), dict(r_max=float("nan")),
-                                dict(q_strips=-1)])
+                                dict(q_strips=-1), dict(flags=4)])
 def test_bad_params_are_rejected(lib, kw):
     with pytest.raises(sp.SpectralError) as e:
         sp.spectral_workspace_bytes(_shape(), _params(**kw))
@@ -91,3 +91,21 @@ def test_null_arguments(lib):
 def test_padded_rows_are_accepted(lib):
     # d = 250 with a padded row stride of 256 elements: rows 512-byte aligned
     assert sp.spectral_workspace_bytes(_shape(d_model=250, ld=256), _params()) > 0
+
+
+def test_gram_form_workspace_and_limits(lib):
+    base = sp.spectral_workspace_bytes(_shape(), _params())
+    gram = sp.spectral_workspace_bytes(_shape(), _params(flags=sp.SN_FLAG_GRAM))
+    # Gram partials: 2 d_h (d_h + 16) bytes per query / key head and strip, plus the final z, y
+    units = 2 * (8 + 2)
+    assert gram - base >= units * 2 * 64 * (64 + 16) + 2 * 8 * 2 * 64 * 4
+    with pytest.raises(sp.SpectralError) as e:
+        sp.spectral_workspace_bytes(_shape(head_dim=8), _params(flags=sp.SN_FLAG_GRAM))
+    assert e.value.code == sp.SN_EINVAL and "Gram" in sp.spectral_last_error()
+
+
+def test_row_block_size_limit(lib):
+    # d_h * ld * element size must stay below 2^31 bytes (32-bit buffer offsets)
+    with pytest.raises(sp.SpectralError) as e:
+        sp.spectral_workspace_bytes(_shape(head_dim=128, d_model=1 << 23, ld=1 << 23), _params())
+    assert e.value.code == sp.SN_EINVAL

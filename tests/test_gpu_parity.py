@@ -2,8 +2,10 @@
 
 Bar: relative error <= 1e-3 on every sigma_h and every layer scale, on the
 very weight bits and start vectors the GPU consumed; iteration counts equal
-(fixed count) or within one step (tolerance mode, where fp32 and fp64 may
-cross the threshold one step apart)."""
+(fixed count) or a valid stopping step of the oracle's own sigma sequence
+(tolerance mode).  Both forms of the iteration are held to it: the sweep
+chain (default) and the Gram form (flag SN_FLAG_GRAM), which computes the
+same iterates through the d_h x d_h Gram matrices."""
 
 import math
 
@@ -22,6 +24,15 @@ if not torch.cuda.is_available():  # pragma: no cover - collected on CPU machines, 
     pytest.skip("needs a GPU", allow_module_level=True)
 
 from paper_2602_18851_amd import Spectral  # noqa: E402
+from paper_2602_18851_amd.spectral import SN_FLAG_GRAM  # noqa: E402
+
+FORMS = {"chain": 0, "gram": SN_FLAG_GRAM}
+
+
+def _form_flags(form, head_dim):
+    if form == "gram" and head_dim < 16:
+        pytest.skip("the Gram form needs head_dim >= 16")
+    return FORMS[form]
 
 
 def _rel(a, b):
@@ -83,11 +94,13 @@ def _np(w):
     return w.float().numpy()
 
 
+@pytest.mark.parametrize("form", FORMS)
 @pytest.mark.parametrize("key", ["tiny", "gpt2-small"])
-def test_fp32_configs_all_heads(key):
+def test_fp32_configs_all_heads(key, form):
     wl = WORKLOADS[key]
+    flags = _form_flags(form, wl.head_dim)
     wq, wk, v0, gq, gk = _cpu_case(wl)
-    gpu = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True)
+    gpu = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True, flags=flags)
     check_against_oracle(wl, _np(wq), _np(wk), v0, wl.n_iter, gpu, want_u=True)
 
 
@@ -114,18 +127,21 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("form", FORMS)
 @pytest.mark.parametrize("name,over,ld,strips", CASES, ids=[c[0] for c in CASES])
-def test_shapes_against_oracle(name, over, ld, strips):
+def test_shapes_against_oracle(name, over, ld, strips, form):
+    strips = dict(strips, flags=strips.get("flags", 0) | _form_flags(form, over["head_dim"]))
     wl = WORKLOADS["llama2-70b-gqa"].replace(key=name, n_iter=11, std=0.02, **over)
     wq, wk, v0, gq, gk = _cpu_case(wl, ld)
     gpu = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True, ld=ld or 0, **strips)
     check_against_oracle(wl, _np(wq), _np(wk), v0, wl.n_iter, gpu, want_u=True)
 
 
-def test_tolerance_mode_on_planted_spectra():
+@pytest.mark.parametrize("form", FORMS)
+def test_tolerance_mode_on_planted_spectra(form):
     wl = WORKLOADS["llama2-70b-perstep"].replace(n_layers=2, d_model=256, n_q=4, n_kv=2, head_dim=16)
     wq, wk, v0, gq, gk = _cpu_case(wl)
-    gpu = run_gpu(wl, gq, gk, v0, 2000, tol=1e-4, want_u=True)
+    gpu = run_gpu(wl, gq, gk, v0, 2000, tol=1e-4, want_u=True, flags=FORMS[form])
     assert gpu["iters"].min() >= 2 and gpu["iters"].max() < 2000
     for l in range(wl.n_layers):
         for h in range(wl.n_q):
@@ -134,15 +150,17 @@ def test_tolerance_mode_on_planted_spectra():
                                   1e-4, 2000)
 
 
-def test_one_step_and_short_runs():
+@pytest.mark.parametrize("form", FORMS)
+def test_one_step_and_short_runs(form):
     wl = WORKLOADS["gpt2-small"].replace(n_layers=2)
     wq, wk, v0, gq, gk = _cpu_case(wl)
     for n in (1, 2, 3):
-        gpu = run_gpu(wl, gq, gk, v0, n, want_u=True)
+        gpu = run_gpu(wl, gq, gk, v0, n, want_u=True, flags=FORMS[form])
         check_against_oracle(wl, _np(wq), _np(wk), v0, n, gpu, want_u=True)
 
 
-def test_degenerate_heads():
+@pytest.mark.parametrize("form", FORMS)
+def test_degenerate_heads(form):
     wl = WORKLOADS["llama2-70b-gqa"].replace(key="degenerate", n_layers=2, d_model=256, n_q=4, n_kv=2,
                                              head_dim=32, n_iter=6)
     wq, wk = all_weights(wl, "cpu")
@@ -150,7 +168,7 @@ def test_degenerate_heads():
     v0 = start_vectors(wl, "cpu")
     v0[0, 1] = 0.0                        # zero start vector
     v0[0, 2, 5] = float("nan")            # non-finite start vector
-    gpu = run_gpu(wl, wq.cuda(), wk.cuda(), v0, wl.n_iter, want_u=True)
+    gpu = run_gpu(wl, wq.cuda(), wk.cuda(), v0, wl.n_iter, want_u=True, flags=FORMS[form])
     ref = oracle_step(_np(wq), _np(wk), v0.double().numpy(), wl.n_iter, n_kv=2, head_dim=32, alpha=wl.alpha,
                       want_u=True)
     np.testing.assert_array_equal(gpu["iters"], ref["iters"])
@@ -166,19 +184,21 @@ def test_degenerate_heads():
     assert _rel(gpu["scale"][1], ref["scale"][1]) <= RTOL
 
 
-def test_bitwise_deterministic():
+@pytest.mark.parametrize("form", FORMS)
+def test_bitwise_deterministic(form):
     wl = WORKLOADS["llama2-70b-gqa"].replace(n_layers=2, d_model=1024, n_q=16, n_kv=2, n_iter=7)
     wq, wk, v0, gq, gk = _cpu_case(wl)
-    a = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True)
-    b = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True)
+    a = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True, flags=FORMS[form])
+    b = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True, flags=FORMS[form])
     for k in ("sigma", "scale", "v", "u", "iters"):
         np.testing.assert_array_equal(a[k], b[k])
 
 
-def test_warm_start_continues_the_iteration():
+@pytest.mark.parametrize("form", FORMS)
+def test_warm_start_continues_the_iteration(form):
     wl = WORKLOADS["gpt2-xl"].replace(n_layers=2, n_q=5, n_kv=5)
     wq, wk, v0, gq, gk = _cpu_case(wl)
-    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha)
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, flags=FORMS[form])
     v = v0.cuda()
     est.step(gq, gk, v, 10)
     sigma, _, _ = est.step(gq, gk, v, 10)
@@ -189,12 +209,13 @@ def test_warm_start_continues_the_iteration():
     est.close()
 
 
-def test_homogeneity_of_the_gpu_path():
+@pytest.mark.parametrize("form", FORMS)
+def test_homogeneity_of_the_gpu_path(form):
     """x4 on every attention weight -> sigma and scale x16 (powers of two are exact)."""
     wl = WORKLOADS["gpt2-xl"].replace(n_layers=2, n_q=5, n_kv=5, n_iter=8)
     wq, wk, v0, gq, gk = _cpu_case(wl)
-    a = run_gpu(wl, gq, gk, v0, wl.n_iter)
-    b = run_gpu(wl, gq * 4, gk * 4, v0, wl.n_iter)
+    a = run_gpu(wl, gq, gk, v0, wl.n_iter, flags=FORMS[form])
+    b = run_gpu(wl, gq * 4, gk * 4, v0, wl.n_iter, flags=FORMS[form])
     np.testing.assert_array_equal(b["sigma"], 16 * a["sigma"])
     assert _rel(b["scale"], 16 * a["scale"]).max() < 1e-6
 
@@ -241,8 +262,8 @@ def _check_sampled(wl, gq, gk, v0, n_iter, gpu, heads, tol=0.0):
     print(f"{wl.key}: {len(heads)} sampled heads, max rel err sigma {worst:.3e}")
 
 
-def _run_full(wl, gq, gk, v0, n_iter, tol=0.0):
-    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=tol)
+def _run_full(wl, gq, gk, v0, n_iter, tol=0.0, flags=0):
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=tol, flags=flags)
     v = v0.clone()
     sigma, scale, iters = est.step(gq, gk, v, n_iter)
     torch.cuda.synchronize()
@@ -252,12 +273,13 @@ def _run_full(wl, gq, gk, v0, n_iter, tol=0.0):
     return out
 
 
+@pytest.mark.parametrize("form", FORMS)
 @pytest.mark.parametrize("key", ["gpt2-xl", "llama2-7b-spiked", "llama2-70b-gqa"])
-def test_full_size_sampled(key):
+def test_full_size_sampled(key, form):
     wl = WORKLOADS[key]
     gq, gk = all_weights(wl, "cuda")
     v0 = start_vectors(wl, "cuda")
-    gpu = _run_full(wl, gq, gk, v0, wl.n_iter)
+    gpu = _run_full(wl, gq, gk, v0, wl.n_iter, flags=FORMS[form])
     assert np.isfinite(gpu["sigma"]).all() and (gpu["iters"] == wl.n_iter).all()
     rng = np.random.default_rng(wl.cfg_id)
     heads = _sampled_heads(wl, rng, [0, wl.n_layers - 1], 2)
@@ -294,7 +316,8 @@ def _check_tolerance_stop(res_gpu_iters, res_gpu_sigma, WQ, WK, v_start, tol, ca
     return r, err
 
 
-def test_full_size_per_step_recompute():
+@pytest.mark.parametrize("form", FORMS)
+def test_full_size_per_step_recompute(form):
     """Cold start to tolerance, perturb the weights, warm start from the
     previous vectors.  The oracle replays both calls from its own vectors; the
     second call is compared where both sides stopped the first call at the
@@ -303,7 +326,8 @@ def test_full_size_per_step_recompute():
     L = wl.n_layers
     gq, gk = all_weights(wl, "cuda")
     v0 = start_vectors(wl, "cuda")
-    est = Spectral(L, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=wl.tol)
+    est = Spectral(L, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=wl.tol,
+                   flags=FORMS[form])
     v = v0.clone()
     s0, _, i0 = est.step(gq, gk, v, wl.n_iter)
     s0, i0 = s0.cpu().numpy().copy(), i0.cpu().numpy().copy()

@@ -45,8 +45,9 @@ def parse():
     p.add_argument("--q-strips", type=int, default=0, help="column strips per head in the W_Q sweep (0 = auto)")
     p.add_argument("--k-strips", type=int, default=0, help="column strips per KV head in the W_K sweep (0 = auto)")
     p.add_argument("--flags", type=int, default=0, help="sn_params.flags (SN_FLAG_* bits)")
-    p.add_argument("--form", choices=("chain", "gram"), default="chain",
-                   help="gram: the Gram form of the iteration (adds SN_FLAG_GRAM)")
+    p.add_argument("--form", choices=("chain", "gram", "layer"), default="chain",
+                   help="gram: the Gram form of the iteration (adds SN_FLAG_GRAM); layer: the paper-literal "
+                        "layer-level estimator (one u, v per layer, spectral_step_layer)")
     p.add_argument("--mode", choices=("bench", "copy"), default="bench",
                    help="copy: one plain device copy of --copy-bytes, the reference for HBM byte counters")
     p.add_argument("--copy-bytes", type=int, default=4 << 30)
@@ -127,27 +128,31 @@ def main():
     import torch
 
     from paper_2602_18851_amd import Spectral
-    from paper_2602_18851_amd.spectral import SN_FLAG_GRAM
-    from workloads import WORKLOADS, all_weights, start_vectors
+    from paper_2602_18851_amd.spectral import SN_FLAG_GRAM, SN_FLAG_LAYER
+    from workloads import WORKLOADS, all_weights, layer_start_vectors, start_vectors
 
     wl = WORKLOADS[args.workload]
     n_iter = args.n_iter or wl.n_iter
     torch.cuda.set_device(0)
     dev = torch.device("cuda", 0)
     wq, wk = all_weights(wl, dev)
-    v0 = start_vectors(wl, dev)
+    layer = args.form == "layer"
+    v0 = layer_start_vectors(wl, dev) if layer else start_vectors(wl, dev)
     v = v0.clone()
-    sigma = torch.empty(wl.n_layers, wl.n_q, dtype=torch.float32, device=dev)
+    sigma = torch.empty(wl.n_layers, *([] if layer else [wl.n_q]), dtype=torch.float32, device=dev)
     scale = torch.empty(wl.n_layers, dtype=torch.float32, device=dev)
     iters = torch.empty(wl.n_layers, wl.n_q, dtype=torch.int32, device=dev)
     gram = args.form == "gram"
-    flags = args.flags | (SN_FLAG_GRAM if gram else 0)
+    flags = args.flags | (SN_FLAG_GRAM if gram else 0) | (SN_FLAG_LAYER if layer else 0)
     est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=0.0,
                    q_strips=args.q_strips, k_strips=args.k_strips, flags=flags)
     torch.cuda.synchronize()
 
     def step():
-        est.step(wq, wk, v, n_iter, sigma=sigma, scale=scale, iters=iters)
+        if layer:
+            est.step_layer(wq, wk, v, n_iter, sigma=sigma, scale=scale)
+        else:
+            est.step(wq, wk, v, n_iter, sigma=sigma, scale=scale, iters=iters)
 
     for _ in range(args.warmup):
         step()
@@ -162,7 +167,7 @@ def main():
     torch.cuda.synchronize()
     wall_s = time.perf_counter() - t_wall
     ms = e0.elapsed_time(e1) / args.steps
-    assert bool(torch.isfinite(sigma).all()) and bool((iters == n_iter).all())
+    assert bool(torch.isfinite(sigma).all()) and (layer or bool((iters == n_iter).all()))
 
     # per-kernel durations, HIP events on the launch stream (separate pass)
     est.profile(True)
@@ -171,7 +176,24 @@ def main():
     est.profile(False)
     H = wl.n_layers * wl.n_q
     q_bytes, k_bytes = wl.weight_bytes()
-    if gram:
+    dom_launch_bytes = None
+    if layer:
+        # per step: row sweeps over W_K and W_Q; column sweeps over W_Q and W_K that
+        # write one d-vector per query / key head; the per-layer sums read them back
+        col_buf = (H + wl.n_layers * wl.n_kv) * wl.d_model * 4
+        r_ms, r_n = prof["layer_row_sweeps"]
+        c_ms, c_n = prof["layer_col_sweeps"]
+        if r_ms >= c_ms:
+            dom_name, dom_kind, dom_alg = "layer_row_sweeps (W_K and W_Q, row sums)", "layer_row_sweeps", \
+                n_iter * (q_bytes + k_bytes)
+        else:
+            dom_name, dom_kind, dom_alg = "layer_col_sweeps (W_Q and W_K, column sums)", "layer_col_sweeps", \
+                n_iter * (q_bytes + k_bytes + col_buf)
+        dom_launch_bytes = dom_alg  # all launches of the kind together
+        dom_flops = None
+        call_bytes = n_iter * (2 * (q_bytes + k_bytes) + 2 * col_buf) + 12 * wl.d_model * wl.n_layers
+        H = wl.n_layers  # one estimate per layer
+    elif gram:
         # Gram sweep: every weight read once, the upper-triangle 16 x 16 Gram
         # blocks written once per query / key head (d_h (d_h + 16) / 2 floats)
         units = H + wl.n_layers * wl.n_kv
@@ -188,12 +210,14 @@ def main():
         call_bytes = n_iter * (q_bytes + k_bytes) + k_bytes + 12 * wl.d_model * H
     dom_ms, dom_n = prof[dom_kind]
     dom_avg_ms = dom_ms / dom_n
+    if dom_launch_bytes is not None:
+        dom_alg = dom_launch_bytes / dom_n  # average algorithmic bytes per launch of the kind
     achieved = dom_alg / (dom_avg_ms * 1e-3) / 1e9
     heads_iters = H * n_iter
     out = {
         "metric": METRIC,
         "value": heads_iters / (ms * 1e-3),
-        "unit": "heads·iters/s",
+        "unit": "layers·iters/s" if layer else "heads·iters/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
@@ -223,7 +247,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": None if gram else measured_traffic(dom_alg),
+            "traffic": None if (gram or layer) else measured_traffic(dom_alg),
             "algorithmic_bytes_per_launch": dom_alg,
             "avg_launch_ms": dom_avg_ms,
             "launches": dom_n,

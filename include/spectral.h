@@ -101,6 +101,11 @@ typedef struct {
  * and column strip (spectral_workspace_bytes gives the total). */
 #define SN_FLAG_GRAM 2
 
+/* Reserve the workspace of the layer-level form (spectral_step_layer):
+ * about (n_layers * n_q * d_model + 2 * n_layers * d_model) * 4 bytes more.
+ * spectral_step itself is unaffected. */
+#define SN_FLAG_LAYER 4
+
 
 typedef struct sn_ctx sn_ctx;
 
@@ -138,6 +143,29 @@ SN_API int spectral_step(sn_ctx* ctx, const void* const* wq_layers, const void* 
                          float* v, float* u, int32_t n_iter, float* sigma, float* scale,
                          int32_t* iters);
 
+/* The layer-level estimator exactly as the paper prints it (App. E,
+ * "Implicit GQA Power Iteration"; g = 1 is the multi-head algorithm of
+ * Sec. 4.1): one pair u, v in R^d per layer for the concatenated
+ * W^Q = [W^Q_1 .. W^Q_{n_q}] and the key weights expanded implicitly,
+ *     z = RepeatBlocks(W^{K T} v, g),  u' = W^Q z,  sigma = ||u'||,
+ *     y = W^{Q T} u,  v' = W^K SumGroups(y, g),  v = v'/||v'||,
+ * so sigma estimates || sum_h W^Q_h W^{K T}_{g(h)} ||_2 for the whole layer
+ * (not max_h of the per-head norms that spectral_step returns).  Needs a
+ * context created with SN_FLAG_LAYER (else SN_ESTATE).
+ *   wq_layers, wk_layers  as for spectral_step.
+ *   v      device float32 [n_layers][d_model], in/out: the persistent right
+ *          vector of each layer (normalised on entry, unit vector on exit).
+ *   u      device float32 [n_layers][d_model] or NULL: the unit left vector.
+ *   n_iter >= 1 iterations (fixed count; params.tol does not apply).
+ *   sigma  device float32 [n_layers]: the estimate of the last step.
+ *   scale  device float32 [n_layers]: Eq. "scale" with that sigma.
+ * A layer whose start vector is zero or not finite gets sigma = scale = NaN,
+ * v unchanged and u = 0; one with M v = 0 gets sigma = scale = 0, v the
+ * normalised start vector and u = 0.  Queued on the context's stream; never
+ * waits.  Errors: SN_ENULL, SN_EINVAL, SN_ESTATE, SN_EHIP. */
+SN_API int spectral_step_layer(sn_ctx* ctx, const void* const* wq_layers, const void* const* wk_layers,
+                               float* v, float* u, int32_t n_iter, float* sigma, float* scale);
+
 /* Redirects later calls to another hipStream_t. */
 SN_API int spectral_set_stream(sn_ctx* ctx, void* hip_stream);
 
@@ -155,11 +183,13 @@ SN_API int spectral_workspace_bytes(const sn_shape* shape, const sn_params* para
  * HIP events on the context's stream.  spectral_profile_read waits for the
  * stream and returns, per kernel kind (0 = first W_K sweep from v,
  * 1 = W_Q sweep, 2 = W_K sweep, 3 = finalize, 4 = Gram sweep, 5 = d_h-space
- * iteration, 6 = final sweeps of the Gram form), the summed device time in
+ * iteration, 6 = final sweeps of the Gram form, 7 = row sweeps of the
+ * layer-level form, 8 = its column sweeps, 9 = its reductions and
+ * finalize), the summed device time in
  * milliseconds and the number of launches since the previous read, then
  * resets both.  ms and launches point to SN_PROFILE_KINDS host elements
  * each. */
-#define SN_PROFILE_KINDS 7
+#define SN_PROFILE_KINDS 10
 SN_API int spectral_profile(sn_ctx* ctx, int32_t enable);
 SN_API int spectral_profile_read(sn_ctx* ctx, double* ms, int64_t* launches);
 

@@ -7,6 +7,8 @@ from .spectral import (  # noqa: F401
     LIB_PATH,
     SN_BF16,
     SN_F32,
+    SN_FLAG_GRAM,
+    SN_FLAG_LAYER,
     SN_FLAG_VALU_K_SWEEP,
     Spectral,
     SpectralError,
@@ -24,5 +26,6 @@ from .spectral import (  # noqa: F401
     spectral_profile_read,
     spectral_set_stream,
     spectral_step,
+    spectral_step_layer,
     spectral_workspace_bytes,
 )

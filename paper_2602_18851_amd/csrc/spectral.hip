@@ -74,7 +74,10 @@ constexpr int kStreamPolicy = 2;       // cache policy of the weight loads: non-
 // and the two final sweeps of the Gram form (v' = K_j^T y and u' = Q_h^T z
 // from the d_h-vectors the Gram iteration leaves behind).
 enum { PH_INIT = 0, PH_Q = 1, PH_K = 2, PH_EK = 3, PH_EQ = 4 };
-enum { KIND_INIT = 0, KIND_Q = 1, KIND_K = 2, KIND_FIN = 3, KIND_GRAM = 4, KIND_ITER = 5, KIND_EMIT = 6, KIND_N = 7 };
+enum {
+  KIND_INIT = 0, KIND_Q = 1, KIND_K = 2, KIND_FIN = 3, KIND_GRAM = 4, KIND_ITER = 5, KIND_EMIT = 6,
+  KIND_LROWS = 7, KIND_LCOLS = 8, KIND_LRED = 9, KIND_N = 10
+};
 static_assert(KIND_N == SN_PROFILE_KINDS, "profile kinds");
 
 struct Work {
@@ -148,6 +151,13 @@ __device__ __forceinline__ float elem<uint16_t>(const u32x4& q, int c) {
 __device__ __forceinline__ void reuse_fence(u32x4& q) { asm volatile("" : "+v"(q)); }
 
 __device__ __forceinline__ float xor_sum(float x, int m) { return x + __shfl_xor(x, m); }
+
+// Sum over the 64 lanes of a wave (butterfly: every lane gets the same bits).
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m);
+  return x;
+}
 
 // Occupancy floor per SIMD: the accumulators grow with GC * DH / 8 floats.
 template <int DH, int GC>
@@ -1059,6 +1069,227 @@ __global__ void __launch_bounds__(IterShape<DH>::NT) gram_iterate_kernel(IterArg
   }
 }
 
+// ---------------------------------------------------------------------------
+// Layer-level form (spectral_step_layer): the estimator as printed in App. E,
+// one pair u, v in R^d per layer for the concatenated W^Q = [W^Q_1 .. W^Q_nq]
+// and the key blocks repeated per group (RepeatBlocks) on the way in and
+// summed per group (SumGroups) on the way back.  One step is four sweeps:
+//   rows(W_K, v):  z_j = K_j v                     (row sums, per key head)
+//   cols(W_Q, z):  c_h = Q_h^T z_{j(h)}            (column sums, per query head)
+//   u' = sum_h c_h, sigma = ||u'||                 (layer_reduce_kernel)
+//   rows(W_Q, u):  y_h = Q_h u'/sigma
+//   cols(W_K, y):  c_j = K_j^T sum_{h in group j} y_h
+//   v' = sum_j c_j                                 (layer_reduce_kernel)
+// A column sweep item owns whole columns of its unit, so it writes its part
+// of c without partials; the per-layer sum over units runs in a fixed order.
+// Per-layer status: 0 running, -1 start vector zero or not finite, -2 M v = 0.
+enum { LM_ROWS = 0, LM_COLS = 1 };
+
+struct LayerArgs {
+  const void* const* mats;  // device table of this matrix's per-layer pointers
+  int64_t ld;
+  int32_t d, units, n_items, s_out, tps, n_tiles;
+  const int32_t* lstat;     // [L]
+  // rows sweep: x = xvec[layer] / sqrt(xn2[layer]) -> rowpart [L*units][s_out][DH]
+  const float* xvec;
+  const float* xn2;
+  float* rowpart;
+  // cols sweep: y = sum over y_cnt source units starting at (ul / y_div) * y_cnt
+  // of the source rows sweep's partials (y_units per layer, y_strips strips)
+  const float* ypart;
+  int32_t y_units, y_strips, y_div, y_cnt;
+  float* colout;            // [L*units][d]
+};
+
+template <typename T, int DH, int MODE>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4)))
+layer_sweep_kernel(LayerArgs a) {
+  constexpr int VEC = Traits<T>::VEC;
+  constexpr int CPL = kCPL;
+  constexpr int RPL = DH / kRG;
+  constexpr int TILE_C = CPL * VEC;
+  constexpr int ES = sizeof(T);
+  __shared__ float xs[kWaves][DH];
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int chunk = lane % CPL, rg = lane / CPL;
+  const int item = blockIdx.x * kWaves + wv;
+  const bool in_range = item < a.n_items;
+  const int unit = in_range ? item / a.s_out : 0;
+  const int strip = in_range ? item % a.s_out : 0;
+  const int layer = unit / a.units, ul = unit % a.units;
+  const bool valid = in_range && uni(a.lstat[layer]) == 0;
+  if (MODE == LM_COLS && valid) {
+    const int src0 = layer * a.y_units + (ul / a.y_div) * a.y_cnt;
+    for (int r = lane; r < DH; r += 64) {
+      float s = 0.f;
+      for (int i = 0; i < a.y_cnt; ++i)
+        for (int st = 0; st < a.y_strips; ++st) s += a.ypart[((size_t)(src0 + i) * a.y_strips + st) * DH + r];
+      xs[wv][r] = s;
+    }
+  }
+  __syncthreads();
+  if (!valid) return;
+
+  const char* blk = uni(a.mats[layer]) + (int64_t)ul * DH * a.ld * ES;
+  const uint32_t nrec = (uint32_t)((((int64_t)(DH - 1) * a.ld + a.d) * ES + 15) & ~int64_t(15));
+  const __amdgpu_buffer_rsrc_t rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(blk), (short)0, (int)nrec, kRsrcWord3);
+  const uint32_t lane_off = (uint32_t)(((int64_t)rg * RPL * a.ld + chunk * VEC) * ES);
+  const uint32_t row_bytes = (uint32_t)(a.ld * ES);
+
+  float yr[MODE == LM_COLS ? RPL : 1];
+  if (MODE == LM_COLS) {
+#pragma unroll
+    for (int rr = 0; rr < (MODE == LM_COLS ? RPL : 1); ++rr) yr[rr] = xs[wv][rg * RPL + rr];
+  }
+  const float* xrow = a.xvec + (size_t)layer * a.d;
+  float acc[RPL];
+#pragma unroll
+  for (int rr = 0; rr < RPL; ++rr) acc[rr] = 0.f;
+
+  const int n_full = a.d / TILE_C;
+  const int t0 = strip * a.tps;
+  const int t1 = min(t0 + a.tps, a.n_tiles);
+#pragma unroll 1
+  for (int t = t0; t < t1; ++t) {
+    u32x4 tile[RPL];
+    const uint32_t voff = lane_off + (uint32_t)(t * TILE_C * ES);
+#pragma unroll
+    for (int rr = 0; rr < RPL; ++rr)
+      tile[rr] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, rr * row_bytes, kStreamPolicy);
+    const int col = t * TILE_C + chunk * VEC;
+    const int nval = a.d - col;  // >= VEC on full tiles
+    if (t >= n_full) {
+      u32x4 m;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (VEC == 8)
+          m[q] = (2 * q < nval ? 0x0000ffffu : 0u) | (2 * q + 1 < nval ? 0xffff0000u : 0u);
+        else
+          m[q] = q < nval ? 0xffffffffu : 0u;
+      }
+#pragma unroll
+      for (int rr = 0; rr < RPL; ++rr) tile[rr] &= m;
+    }
+    if (MODE == LM_ROWS) {
+      float xv[VEC];
+#pragma unroll
+      for (int c = 0; c < VEC; ++c) xv[c] = c < nval ? xrow[min(col + c, a.d - 1)] : 0.f;
+#pragma unroll
+      for (int rr = 0; rr < RPL; ++rr) {
+        float s = acc[rr];
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) s = fmaf(elem<T>(tile[rr], c), xv[c], s);
+        acc[rr] = s;
+      }
+    } else {
+      float w[VEC];
+#pragma unroll
+      for (int c = 0; c < VEC; ++c) w[c] = 0.f;
+#pragma unroll
+      for (int rr = 0; rr < RPL; ++rr)
+#pragma unroll
+        for (int c = 0; c < VEC; ++c) w[c] = fmaf(elem<T>(tile[rr], c), yr[MODE == LM_COLS ? rr : 0], w[c]);
+#pragma unroll
+      for (int c = 0; c < VEC; ++c) w[c] = group_sum(w[c]);
+      if (rg == 0) {
+        float* out = a.colout + (size_t)unit * a.d + col;
+#pragma unroll
+        for (int c = 0; c < VEC; ++c)
+          if (c < nval) out[c] = w[c];
+      }
+    }
+  }
+  if (MODE == LM_ROWS) {
+    const float xs_inv = 1.0f / sqrtf(a.xn2[layer]);
+    float* op = a.rowpart + ((size_t)unit * a.s_out + strip) * DH + rg * RPL;
+#pragma unroll
+    for (int rr = 0; rr < RPL; ++rr) {
+      float s = acc[rr];
+#pragma unroll
+      for (int m = 1; m < CPL; m <<= 1) s = xor_sum(s, m);
+      if ((rr % CPL) == chunk) op[rr] = s * xs_inv;
+    }
+  }
+}
+
+// Per layer: vec[c] = sum over the layer's units of col[unit][c] (fixed order)
+// and n2 = ||vec||^2; mode 0 copies the caller's start vector instead and
+// (re)initialises the layer status; mode 1 marks M v = 0.
+struct LayerReduceArgs {
+  const float* col;
+  int32_t units, d, mode;
+  float* vec;
+  float* n2;
+  float* n2_start;  // mode 0: ||v||^2 of the start vector
+  int32_t* lstat;
+};
+
+constexpr int kRedThreads = 512;
+
+__global__ void __launch_bounds__(kRedThreads) layer_reduce_kernel(LayerReduceArgs r) {
+  const int l = blockIdx.x, t = threadIdx.x;
+  __shared__ float red[kRedThreads / 64];
+  if (r.mode != 0 && r.lstat[l] != 0) return;
+  float acc = 0.f;
+  const float* base = r.col + (size_t)l * r.units * r.d;
+  for (int c = t; c < r.d; c += kRedThreads) {
+    float s = 0.f;
+    for (int u = 0; u < r.units; ++u) s += base[(size_t)u * r.d + c];
+    r.vec[(size_t)l * r.d + c] = s;
+    acc = fmaf(s, s, acc);
+  }
+  acc = wave_sum(acc);
+  if ((t & 63) == 0) red[t >> 6] = acc;
+  __syncthreads();
+  if (t == 0) {
+    const float n2 = sum_waves<kRedThreads / 64>(red);
+    r.n2[l] = n2;
+    if (r.mode == 0) {
+      r.n2_start[l] = n2;
+      r.lstat[l] = (n2 > 0.f && isfinite(n2)) ? 0 : -1;
+    } else if (r.mode == 1 && n2 == 0.f) {
+      r.lstat[l] = -2;
+    }
+  }
+}
+
+// Outputs of the layer-level form: sigma, scale, v = v'/||v'||, u = u'/sigma.
+struct LayerFinArgs {
+  int32_t d, L;
+  float coef;
+  const int32_t* lstat;
+  const float* lu;
+  const float* lv;
+  const float* n2_u;
+  const float* n2_v;
+  const float* n2_start;
+  float* v;
+  float* u;
+  float* sigma;
+  float* scale;
+};
+
+__global__ void __launch_bounds__(kThreads) layer_finalize_kernel(LayerFinArgs f) {
+  const int l = blockIdx.x;
+  const int st = f.lstat[l];
+  const float sig = st == -1 ? __builtin_nanf("") : st == -2 ? 0.f : sqrtf(f.n2_u[l]);
+  if (threadIdx.x == 0) {
+    f.sigma[l] = sig;
+    f.scale[l] = f.coef * sig;
+  }
+  float* vp = f.v + (size_t)l * f.d;
+  float* up = f.u ? f.u + (size_t)l * f.d : nullptr;
+  const float vs = st == 0 ? 1.0f / sqrtf(f.n2_v[l]) : st == -2 ? 1.0f / sqrtf(f.n2_start[l]) : 1.f;
+  const float us = st == 0 ? 1.0f / sig : 0.f;
+  for (int c = threadIdx.x; c < f.d; c += blockDim.x) {
+    if (st == 0) vp[c] = f.lv[(size_t)l * f.d + c] * vs;
+    else if (st == -2) vp[c] *= vs;
+    if (up) up[c] = st == 0 ? f.lu[(size_t)l * f.d + c] * us : 0.f;
+  }
+}
+
 // Normalises the final vectors and computes the per-layer scale.
 // Blocks [0, H): one head each; blocks [H, H + L): one layer each.
 __global__ void __launch_bounds__(kThreads) finalize_kernel(FinArgs f) {
@@ -1115,7 +1346,11 @@ struct Plan {
   int s_q, tps_q, s_k, tps_k;
   bool gram;    // Gram form
   int units_g, s_g, tps_g, n_tiles_g, nb_g;
-  size_t off_zp, off_zn, off_yp, off_yn, off_sig, off_vn, off_alive, off_nalive, off_iters, off_fin, off_gp, bytes;
+  bool layer;   // layer-level form
+  int s_lq, tps_lq, s_lk, tps_lk;  // row / column strips of the layer-form sweeps over W_Q and W_K
+  size_t off_zp, off_zn, off_yp, off_yn, off_sig, off_vn, off_alive, off_nalive, off_iters, off_fin, off_gp;
+  size_t off_lz, off_ly, off_lcol, off_lu, off_lv, off_ln2, off_lstat;
+  size_t bytes;
 };
 
 int esize(int dtype) { return dtype == SN_F32 ? 4 : 2; }
@@ -1140,7 +1375,7 @@ int validate(const sn_shape* s, const sn_params* p) {
     return fail(SN_EINVAL, "alpha, eta_fp8 and r_max must be finite and > 0");
   if (!(p->tol >= 0.f) || !std::isfinite(p->tol)) return fail(SN_EINVAL, "tol must be finite and >= 0");
   if (p->q_strips < 0 || p->k_strips < 0) return fail(SN_EINVAL, "strip counts must be >= 0");
-  if (p->flags & ~(SN_FLAG_VALU_K_SWEEP | SN_FLAG_GRAM)) return fail(SN_EINVAL, "unknown flag bits");
+  if (p->flags & ~(SN_FLAG_VALU_K_SWEEP | SN_FLAG_GRAM | SN_FLAG_LAYER)) return fail(SN_EINVAL, "unknown flag bits");
   if ((p->flags & SN_FLAG_GRAM) && s->head_dim < 16) return fail(SN_EINVAL, "the Gram form needs head_dim >= 16");
   if ((int64_t)s->head_dim * ld * esize(s->dtype) >= (int64_t(1) << 31))
     return fail(SN_EINVAL, "head_dim * ld * element size must be below 2^31 bytes");
@@ -1207,6 +1442,19 @@ Plan make_plan(const sn_shape* s, const sn_params* p) {
   if (pl.gram) {
     pl.off_fin = take(H * 2 * dh * 4);
     pl.off_gp = take((size_t)pl.units_g * pl.s_g * pl.nb_g * 256 * 4);
+  }
+  pl.layer = (p->flags & SN_FLAG_LAYER) != 0;
+  if (pl.layer) {
+    const size_t L = s->n_layers, Hk = L * s->n_kv_heads, d = s->d_model;
+    strips(pl.n_tiles_q, pl.H, 0, kQTargetItems, false, &pl.s_lq, &pl.tps_lq);
+    strips(pl.n_tiles_q, (int64_t)Hk, 0, kQTargetItems, false, &pl.s_lk, &pl.tps_lk);
+    pl.off_lz = take(Hk * pl.s_lk * dh * 4);
+    pl.off_ly = take(H * pl.s_lq * dh * 4);
+    pl.off_lcol = take(H * d * 4);
+    pl.off_lu = take(L * d * 4);
+    pl.off_lv = take(L * d * 4);
+    pl.off_ln2 = take(3 * L * 4);
+    pl.off_lstat = take(L * 4);
   }
   pl.bytes = off;
   return pl;
@@ -1356,6 +1604,92 @@ void gram_dispatch(int dh, dim3 grid, hipStream_t st, const GramArgs& g) {
     case 64: gram_kernel<T, 64><<<grid, 64 * kGWaves, 0, st>>>(g); break;
     default: gram_kernel<T, 128><<<grid, 64 * kGWaves, 0, st>>>(g); break;
   }
+}
+
+// Eq. "scale" per unit of sigma: alpha * d / sqrt(d_h) / (eta_fp8 * r_max), in double.
+float scale_coef(const sn_ctx* c) {
+  return (float)((double)c->params.alpha * (double)c->shape.d_model /
+                 (std::sqrt((double)c->shape.head_dim) * (double)c->params.eta_fp8 * (double)c->params.r_max));
+}
+
+// Checks the layer pointers and the device, and refreshes the device copy of
+// the per-layer pointer table when the pointers changed.
+int update_table(sn_ctx* c, const void* const* wq_layers, const void* const* wk_layers) {
+  const int L = c->shape.n_layers;
+  for (int l = 0; l < L; ++l) {
+    if (!wq_layers[l] || !wk_layers[l]) return fail(SN_ENULL, "a layer weight pointer is NULL");
+    if ((reinterpret_cast<uintptr_t>(wq_layers[l]) | reinterpret_cast<uintptr_t>(wk_layers[l])) & 15)
+      return fail(SN_EINVAL, "layer weight pointers must be 16-byte aligned");
+  }
+  int cur_dev = 0;
+  SN_HIP(hipGetDevice(&cur_dev));
+  if (cur_dev != c->device) return fail(SN_ESTATE, "the current HIP device is not the context's device");
+  bool same = c->cached.size() == (size_t)(2 * L);
+  for (int l = 0; same && l < L; ++l)
+    same = c->cached[l] == wq_layers[l] && c->cached[L + l] == wk_layers[l];
+  if (!same) {
+    SN_HIP(hipEventSynchronize(c->tab_event));  // the staging buffer's previous copy has been read
+    c->cached.assign(2 * L, nullptr);
+    for (int l = 0; l < L; ++l) {
+      c->h_tab[l] = c->cached[l] = wq_layers[l];
+      c->h_tab[L + l] = c->cached[L + l] = wk_layers[l];
+    }
+    SN_HIP(hipMemcpyAsync(c->d_tab, c->h_tab, 2 * L * sizeof(void*), hipMemcpyHostToDevice, c->stream));
+    SN_HIP(hipEventRecord(c->tab_event, c->stream));
+  }
+  return SN_OK;
+}
+
+template <typename T, int MODE>
+void layer_dispatch(int dh, dim3 grid, hipStream_t st, const LayerArgs& a) {
+  switch (dh) {
+    case 8: layer_sweep_kernel<T, 8, MODE><<<grid, kThreads, 0, st>>>(a); break;
+    case 16: layer_sweep_kernel<T, 16, MODE><<<grid, kThreads, 0, st>>>(a); break;
+    case 32: layer_sweep_kernel<T, 32, MODE><<<grid, kThreads, 0, st>>>(a); break;
+    case 64: layer_sweep_kernel<T, 64, MODE><<<grid, kThreads, 0, st>>>(a); break;
+    default: layer_sweep_kernel<T, 128, MODE><<<grid, kThreads, 0, st>>>(a); break;
+  }
+}
+
+// One layer-form sweep over W_Q (q = true) or W_K.
+int layer_sweep(sn_ctx* c, bool q, int mode, LayerArgs a) {
+  const Plan& pl = c->plan;
+  const int L = c->shape.n_layers;
+  a.mats = c->d_tab + (q ? 0 : L);
+  a.ld = c->shape.ld;
+  a.d = c->shape.d_model;
+  a.units = q ? c->shape.n_q_heads : c->shape.n_kv_heads;
+  a.s_out = q ? pl.s_lq : pl.s_lk;
+  a.tps = q ? pl.tps_lq : pl.tps_lk;
+  a.n_tiles = pl.n_tiles_q;
+  a.n_items = L * a.units * a.s_out;
+  a.lstat = reinterpret_cast<const int32_t*>(c->ws + pl.off_lstat);
+  const dim3 grid(ceil_div(a.n_items, kWaves));
+  const int dh = c->shape.head_dim;
+  return timed(c, mode == LM_ROWS ? KIND_LROWS : KIND_LCOLS, [&] {
+    if (c->shape.dtype == SN_BF16) {
+      if (mode == LM_ROWS) layer_dispatch<uint16_t, LM_ROWS>(dh, grid, c->stream, a);
+      else layer_dispatch<uint16_t, LM_COLS>(dh, grid, c->stream, a);
+    } else {
+      if (mode == LM_ROWS) layer_dispatch<float, LM_ROWS>(dh, grid, c->stream, a);
+      else layer_dispatch<float, LM_COLS>(dh, grid, c->stream, a);
+    }
+  });
+}
+
+int layer_reduce(sn_ctx* c, const float* col, int units, int mode, float* vec, float* n2) {
+  const Plan& pl = c->plan;
+  LayerReduceArgs r{};
+  r.col = col;
+  r.units = units;
+  r.d = c->shape.d_model;
+  r.mode = mode;
+  r.vec = vec;
+  r.n2 = n2;
+  r.n2_start = reinterpret_cast<float*>(c->ws + pl.off_ln2) + 2 * c->shape.n_layers;
+  r.lstat = reinterpret_cast<int32_t*>(c->ws + pl.off_lstat);
+  return timed(c, KIND_LRED,
+               [&] { layer_reduce_kernel<<<dim3(c->shape.n_layers), kRedThreads, 0, c->stream>>>(r); });
 }
 
 // The sweeps of the default form: first W_K sweep, then n_iter x (W_Q sweep,
@@ -1552,29 +1886,8 @@ SN_API int spectral_step(sn_ctx* c, const void* const* wq_layers, const void* co
     return fail(SN_ENULL, "wq_layers, wk_layers, v, sigma and scale must not be NULL");
   if (n_iter < 1) return fail(SN_EINVAL, "n_iter must be >= 1");
   const int L = c->shape.n_layers;
-  for (int l = 0; l < L; ++l) {
-    if (!wq_layers[l] || !wk_layers[l]) return fail(SN_ENULL, "a layer weight pointer is NULL");
-    if ((reinterpret_cast<uintptr_t>(wq_layers[l]) | reinterpret_cast<uintptr_t>(wk_layers[l])) & 15)
-      return fail(SN_EINVAL, "layer weight pointers must be 16-byte aligned");
-  }
-  int cur_dev = 0;
-  SN_HIP(hipGetDevice(&cur_dev));
-  if (cur_dev != c->device) return fail(SN_ESTATE, "the current HIP device is not the context's device");
-
-  // device copy of the per-layer pointer table (only when it changed)
-  bool same = c->cached.size() == (size_t)(2 * L);
-  for (int l = 0; same && l < L; ++l)
-    same = c->cached[l] == wq_layers[l] && c->cached[L + l] == wk_layers[l];
-  if (!same) {
-    SN_HIP(hipEventSynchronize(c->tab_event));  // the staging buffer's previous copy has been read
-    c->cached.assign(2 * L, nullptr);
-    for (int l = 0; l < L; ++l) {
-      c->h_tab[l] = c->cached[l] = wq_layers[l];
-      c->h_tab[L + l] = c->cached[L + l] = wk_layers[l];
-    }
-    SN_HIP(hipMemcpyAsync(c->d_tab, c->h_tab, 2 * L * sizeof(void*), hipMemcpyHostToDevice, c->stream));
-    SN_HIP(hipEventRecord(c->tab_event, c->stream));
-  }
+  int rc = update_table(c, wq_layers, wk_layers);
+  if (rc != SN_OK) return rc;
 
   const Plan& pl = c->plan;
   SweepArgs a{};
@@ -1596,7 +1909,7 @@ SN_API int spectral_step(sn_ctx* c, const void* const* wq_layers, const void* co
   a.sigma = sigma;
   a.iters = iters ? iters : c->w.iters;
 
-  const int rc = pl.gram ? run_gram(c, a, u) : run_chain(c, a, u);
+  rc = pl.gram ? run_gram(c, a, u) : run_chain(c, a, u);
   if (rc != SN_OK) return rc;
 
   FinArgs f{};
@@ -1606,8 +1919,7 @@ SN_API int spectral_step(sn_ctx* c, const void* const* wq_layers, const void* co
   f.d = c->shape.d_model;
   f.s_k = pl.s_k;
   f.slot_fixed = pl.gram ? 0 : -1;
-  f.coef = (float)((double)c->params.alpha * (double)c->shape.d_model /
-                   (std::sqrt((double)c->shape.head_dim) * (double)c->params.eta_fp8 * (double)c->params.r_max));
+  f.coef = scale_coef(c);
   f.w = c->w;
   f.v = v;
   f.u = u;
@@ -1615,6 +1927,73 @@ SN_API int spectral_step(sn_ctx* c, const void* const* wq_layers, const void* co
   f.scale = scale;
   f.iters = a.iters;
   return timed(c, KIND_FIN, [&] { finalize_kernel<<<dim3(pl.H + L), kThreads, 0, c->stream>>>(f); });
+}
+
+SN_API int spectral_step_layer(sn_ctx* c, const void* const* wq_layers, const void* const* wk_layers, float* v,
+                               float* u, int32_t n_iter, float* sigma, float* scale) {
+  if (!c) return fail(SN_ENULL, "ctx must not be NULL");
+  if (!wq_layers || !wk_layers || !v || !sigma || !scale)
+    return fail(SN_ENULL, "wq_layers, wk_layers, v, sigma and scale must not be NULL");
+  if (!c->plan.layer) return fail(SN_ESTATE, "the context was created without SN_FLAG_LAYER");
+  if (n_iter < 1) return fail(SN_EINVAL, "n_iter must be >= 1");
+  int rc = update_table(c, wq_layers, wk_layers);
+  if (rc != SN_OK) return rc;
+  const Plan& pl = c->plan;
+  const int L = c->shape.n_layers;
+  float* lz = reinterpret_cast<float*>(c->ws + pl.off_lz);
+  float* ly = reinterpret_cast<float*>(c->ws + pl.off_ly);
+  float* lcol = reinterpret_cast<float*>(c->ws + pl.off_lcol);
+  float* lu = reinterpret_cast<float*>(c->ws + pl.off_lu);
+  float* lv = reinterpret_cast<float*>(c->ws + pl.off_lv);
+  float* n2_u = reinterpret_cast<float*>(c->ws + pl.off_ln2);
+  float* n2_v = n2_u + L;
+  // start vectors: copy, squared norms, layer status
+  if ((rc = layer_reduce(c, v, 1, 0, lv, n2_v)) != SN_OK) return rc;
+  for (int k = 1; k <= n_iter; ++k) {
+    LayerArgs a{};
+    a.xvec = lv;  // z_j = K_j v
+    a.xn2 = n2_v;
+    a.rowpart = lz;
+    if ((rc = layer_sweep(c, false, LM_ROWS, a)) != SN_OK) return rc;
+    a = LayerArgs{};  // c_h = Q_h^T z_{j(h)}: RepeatBlocks
+    a.ypart = lz;
+    a.y_units = c->shape.n_kv_heads;
+    a.y_strips = pl.s_lk;
+    a.y_div = pl.g;
+    a.y_cnt = 1;
+    a.colout = lcol;
+    if ((rc = layer_sweep(c, true, LM_COLS, a)) != SN_OK) return rc;
+    if ((rc = layer_reduce(c, lcol, c->shape.n_q_heads, 1, lu, n2_u)) != SN_OK) return rc;
+    a = LayerArgs{};  // y_h = Q_h u
+    a.xvec = lu;
+    a.xn2 = n2_u;
+    a.rowpart = ly;
+    if ((rc = layer_sweep(c, true, LM_ROWS, a)) != SN_OK) return rc;
+    a = LayerArgs{};  // c_j = K_j^T sum_{h in j} y_h: SumGroups
+    a.ypart = ly;
+    a.y_units = c->shape.n_q_heads;
+    a.y_strips = pl.s_lq;
+    a.y_div = 1;
+    a.y_cnt = pl.g;
+    a.colout = lcol;
+    if ((rc = layer_sweep(c, false, LM_COLS, a)) != SN_OK) return rc;
+    if ((rc = layer_reduce(c, lcol, c->shape.n_kv_heads, 2, lv, n2_v)) != SN_OK) return rc;
+  }
+  LayerFinArgs f{};
+  f.d = c->shape.d_model;
+  f.L = L;
+  f.coef = scale_coef(c);
+  f.lstat = reinterpret_cast<const int32_t*>(c->ws + pl.off_lstat);
+  f.lu = lu;
+  f.lv = lv;
+  f.n2_u = n2_u;
+  f.n2_v = n2_v;
+  f.n2_start = n2_u + 2 * L;
+  f.v = v;
+  f.u = u;
+  f.sigma = sigma;
+  f.scale = scale;
+  return timed(c, KIND_LRED, [&] { layer_finalize_kernel<<<dim3(L), kThreads, 0, c->stream>>>(f); });
 }
 
 }  // extern "C"

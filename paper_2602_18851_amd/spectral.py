@@ -19,12 +19,15 @@ SN_OK, SN_EINVAL, SN_ENULL, SN_EDTYPE, SN_EHIP, SN_ESTATE = 0, -1, -2, -3, -4, -
 SN_F32, SN_BF16 = 0, 1
 SN_FLAG_VALU_K_SWEEP = 1
 SN_FLAG_GRAM = 2
-KIND_NAMES = ("k_sweep_first", "q_sweep", "k_sweep", "finalize", "gram_sweep", "gram_iterate", "gram_final_sweeps")
+SN_FLAG_LAYER = 4
+KIND_NAMES = ("k_sweep_first", "q_sweep", "k_sweep", "finalize", "gram_sweep", "gram_iterate", "gram_final_sweeps",
+              "layer_row_sweeps", "layer_col_sweeps", "layer_reduce")
 SN_PROFILE_KINDS = len(KIND_NAMES)
 
 EXPORTED = (
     "spectral_init",
     "spectral_step",
+    "spectral_step_layer",
     "spectral_set_stream",
     "spectral_destroy",
     "spectral_last_error",
@@ -84,6 +87,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.spectral_init.restype = ctypes.c_int
     lib.spectral_step.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp, i32, vp, vp, vp]
     lib.spectral_step.restype = ctypes.c_int
+    lib.spectral_step_layer.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp, i32, vp, vp]
+    lib.spectral_step_layer.restype = ctypes.c_int
     lib.spectral_set_stream.argtypes = [vp, vp]
     lib.spectral_set_stream.restype = ctypes.c_int
     lib.spectral_destroy.argtypes = [vp]
@@ -144,6 +149,15 @@ def spectral_step(ctx: int, wq_ptrs: Sequence[int], wk_ptrs: Sequence[int], v: i
                                         ctypes.c_void_p(u or None), int(n_iter), ctypes.c_void_p(sigma),
                                         ctypes.c_void_p(scale), ctypes.c_void_p(iters or None)))
 
+
+def spectral_step_layer(ctx: int, wq_ptrs: Sequence[int], wk_ptrs: Sequence[int], v: int, u: int, n_iter: int,
+                        sigma: int, scale: int) -> None:
+    n = len(wq_ptrs)
+    wq = (ctypes.c_void_p * n)(*wq_ptrs)
+    wk = (ctypes.c_void_p * n)(*wk_ptrs)
+    _check(load_library().spectral_step_layer(ctypes.c_void_p(ctx), wq, wk, ctypes.c_void_p(v),
+                                              ctypes.c_void_p(u or None), int(n_iter), ctypes.c_void_p(sigma),
+                                              ctypes.c_void_p(scale)))
 
 def spectral_set_stream(ctx: int, stream: int) -> None:
     _check(load_library().spectral_set_stream(ctypes.c_void_p(ctx), ctypes.c_void_p(stream)))
@@ -276,6 +290,33 @@ class Spectral:
         spectral_step(self.ctx, wq_p, wk_p, v.data_ptr(), u.data_ptr() if u is not None else 0, n_iter,
                       sigma.data_ptr(), scale.data_ptr(), iters.data_ptr())
         return sigma, scale, iters
+
+    def step_layer(self, wq, wk, v, n_iter: int, u=None, sigma=None, scale=None):
+        """Layer-level form (context made with SN_FLAG_LAYER): v, u float32
+        [L, d] (v in/out).  Returns (sigma [L], scale [L])."""
+        import torch
+
+        s = self.shape
+        L, d = s.n_layers, s.d_model
+        wq_p = self._layer_ptrs(wq, s.n_q_heads * s.head_dim)
+        wk_p = self._layer_ptrs(wk, s.n_kv_heads * s.head_dim)
+        for name, t in (("v", v), ("u", u)):
+            if t is None:
+                continue
+            if t.dtype != torch.float32 or tuple(t.shape) != (L, d) or not t.is_contiguous() or not t.is_cuda:
+                raise ValueError(f"{name} must be a contiguous float32 CUDA tensor of shape {(L, d)}")
+        dev = v.device
+        if sigma is None:
+            sigma = torch.empty(L, dtype=torch.float32, device=dev)
+        if scale is None:
+            scale = torch.empty(L, dtype=torch.float32, device=dev)
+        stream = torch.cuda.current_stream(dev).cuda_stream
+        if stream != self._stream:
+            spectral_set_stream(self.ctx, stream)
+            self._stream = stream
+        spectral_step_layer(self.ctx, wq_p, wk_p, v.data_ptr(), u.data_ptr() if u is not None else 0, n_iter,
+                            sigma.data_ptr(), scale.data_ptr())
+        return sigma, scale
 
     def profile(self, enable: bool = True):
         spectral_profile(self.ctx, enable)

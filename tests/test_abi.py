@@ -74,7 +74,7 @@ def test_bad_shapes_are_rejected(lib, kw, code):
 
 
 @pytest.mark.parametrize("kw", [dict(alpha=0.0), dict(eta_fp8=-1.0), dict(tol=-1e-3), dict(r_max=float("nan")),
-                                dict(q_strips=-1), dict(flags=4)])
+                                dict(q_strips=-1), dict(flags=8)])
 def test_bad_params_are_rejected(lib, kw):
     with pytest.raises(sp.SpectralError) as e:
         sp.spectral_workspace_bytes(_shape(), _params(**kw))
@@ -109,3 +109,11 @@ def test_row_block_size_limit(lib):
     with pytest.raises(sp.SpectralError) as e:
         sp.spectral_workspace_bytes(_shape(head_dim=128, d_model=1 << 23, ld=1 << 23), _params())
     assert e.value.code == sp.SN_EINVAL
+
+
+def test_layer_form_needs_its_flag(lib):
+    base = sp.spectral_workspace_bytes(_shape(), _params())
+    lay = sp.spectral_workspace_bytes(_shape(), _params(flags=sp.SN_FLAG_LAYER))
+    # column buffer of every query head plus u', v' per layer
+    assert lay - base >= (2 * 8 * 256 + 2 * 2 * 256) * 4
+    assert lib.spectral_step_layer(None, None, None, None, None, 1, None, None) == sp.SN_ENULL

@@ -11,6 +11,7 @@ from .synth import (  # noqa: F401
     layer_weights,
     all_weights,
     start_vectors,
+    layer_start_vectors,
     perturb_master,
     tokens,
     planted_singular_values,

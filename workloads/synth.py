@@ -36,7 +36,7 @@ import numpy as np
 import torch
 
 SEED_ROOT = 20260218
-STREAMS = {"q": 0, "k": 1, "v0": 2, "u0": 3, "perturb": 4, "x": 5, "plant": 6}
+STREAMS = {"q": 0, "k": 1, "v0": 2, "u0": 3, "perturb": 4, "x": 5, "plant": 6, "v0-layer": 7}
 
 
 @dataclass(frozen=True)
@@ -249,6 +249,15 @@ def start_vectors(wl: Workload, device="cpu") -> torch.Tensor:
     Drawn N(0, I) and normalised in float64 before the float32 store."""
     g = _gen(device, seed_of(wl.cfg_id, 0, "v0"))
     v = torch.randn(wl.n_layers, wl.n_q, wl.d_model, generator=g, device=device, dtype=torch.float64)
+    v /= torch.linalg.vector_norm(v, dim=-1, keepdim=True)
+    return v.to(torch.float32)
+
+
+def layer_start_vectors(wl: Workload, device="cpu") -> torch.Tensor:
+    """Random unit start vectors, one per layer (the layer-level estimator):
+    float32 [L, d], drawn and normalised like ``start_vectors``."""
+    g = _gen(device, seed_of(wl.cfg_id, 0, "v0-layer"))
+    v = torch.randn(wl.n_layers, wl.d_model, generator=g, device=device, dtype=torch.float64)
     v /= torch.linalg.vector_norm(v, dim=-1, keepdim=True)
     return v.to(torch.float32)
 

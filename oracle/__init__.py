@@ -17,6 +17,9 @@ explicit         Textbook cross-checks that form M = W^Q W^{K T} explicitly:
 calibration      Eq. "scale", the gamma / alpha_min selection rule (Sec. 3.2)
                  and the overflow-probability terms T1, T2.
 e4m3             Exact OCP E4M3FN encoder / decoder and the overflow predicate.
+fp8_consumer     Stage 3 of the geometry-aware forward pass up to the E4M3
+                 logits: S = Q K^T / sqrt(d_h), S / scale, codes, max |S~| and
+                 the overflow count per head.
 
 Every function here is pinned by the ``-m "not gpu"`` tests against values
 the paper prints, closed forms or textbook routines; none is "parity

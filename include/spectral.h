@@ -166,6 +166,42 @@ SN_API int spectral_step(sn_ctx* ctx, const void* const* wq_layers, const void* 
 SN_API int spectral_step_layer(sn_ctx* ctx, const void* const* wq_layers, const void* const* wk_layers,
                                float* v, float* u, int32_t n_iter, float* sigma, float* scale);
 
+/* ---- FP8 E4M3 consumer of the scale ----------------------------------
+ *
+ * Stage 3 of the geometry-aware forward pass (Sec. 3.4, Algorithm
+ * "Geometry-Aware Attention Forward Pass") up to the quantised logits, for
+ * every layer l and query head h:
+ *     Q = X_l W^Q,  K = X_l W^K,  S_h = Q_h K_{g(h)}^T / sqrt(d_h),
+ *     S~_h = S_h / scale_l  ->  OCP E4M3FN codes (round to nearest even;
+ *                              |S~| > 464 gives NaN, 0x7F | sign),
+ * with the statistics of Sec. 1 (overflow when |S~| > 448) and Table
+ * "pretrained" (largest scaled logit).  Key heads are not expanded.  The
+ * projections accumulate in fp32 and the logits are formed to about 2^-15
+ * relative precision (three bf16 matrix-core products on hi/lo halves).
+ * Needs bf16 weights and tokens and head_dim 16, 32, 64 or 128.
+ *
+ * spectral_logits_workspace_bytes: device scratch the call needs
+ * (seq_len * (n_q + n_kv) * head_dim * 4 bytes; it holds one layer's Q, K).
+ *
+ * spectral_logits_fp8:
+ *   x_layers   host array of n_layers device pointers: tokens of layer l,
+ *              bf16 [seq_len][ld_x] (ld_x = 0: d_model), 16-byte aligned.
+ *   wq_layers, wk_layers  as for spectral_step.
+ *   scale      device float32 [n_layers] (e.g. spectral_step's output).
+ *   workspace  device scratch of >= workspace_bytes bytes, 256-byte aligned,
+ *              owned by the caller; contents are overwritten.
+ *   codes      device uint8 [n_layers][n_q][seq_len][seq_len] or NULL
+ *              (16-byte aligned): E4M3 codes of S~, row i, column j.
+ *   max_abs    device float32 [n_layers][n_q]: max |S~| per head.
+ *   n_over     device int32 [n_layers][n_q]: #{(i, j): |S~_ij| > 448}.
+ * Queued on the context's stream; allocates nothing; seq_len <= 46340.
+ * Errors: SN_ENULL, SN_EINVAL, SN_EDTYPE, SN_ESTATE. */
+SN_API int spectral_logits_workspace_bytes(const sn_shape* shape, int32_t seq_len, int64_t* bytes);
+SN_API int spectral_logits_fp8(sn_ctx* ctx, const void* const* x_layers, int64_t ld_x, int32_t seq_len,
+                               const void* const* wq_layers, const void* const* wk_layers, const float* scale,
+                               void* workspace, int64_t workspace_bytes, uint8_t* codes, float* max_abs,
+                               int32_t* n_over);
+
 /* Redirects later calls to another hipStream_t. */
 SN_API int spectral_set_stream(sn_ctx* ctx, void* hip_stream);
 
@@ -185,11 +221,12 @@ SN_API int spectral_workspace_bytes(const sn_shape* shape, const sn_params* para
  * 1 = W_Q sweep, 2 = W_K sweep, 3 = finalize, 4 = Gram sweep, 5 = d_h-space
  * iteration, 6 = final sweeps of the Gram form, 7 = row sweeps of the
  * layer-level form, 8 = its column sweeps, 9 = its reductions and
- * finalize), the summed device time in
+ * finalize, 10 = projections of the logit consumer, 11 = its logit
+ * kernels), the summed device time in
  * milliseconds and the number of launches since the previous read, then
  * resets both.  ms and launches point to SN_PROFILE_KINDS host elements
  * each. */
-#define SN_PROFILE_KINDS 10
+#define SN_PROFILE_KINDS 12
 SN_API int spectral_profile(sn_ctx* ctx, int32_t enable);
 SN_API int spectral_profile_read(sn_ctx* ctx, double* ms, int64_t* launches);
 

@@ -22,6 +22,8 @@ from .spectral import (  # noqa: F401
     spectral_slack_ratio,
     spectral_init,
     spectral_last_error,
+    spectral_logits_fp8,
+    spectral_logits_workspace_bytes,
     spectral_profile,
     spectral_profile_read,
     spectral_set_stream,

@@ -12,7 +12,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = [os.path.join(HERE, "csrc", "spectral.hip"), os.path.join(HERE, "csrc", "calibration.cpp")]
+SOURCES = [os.path.join(HERE, "csrc", name) for name in ("spectral.hip", "logits_fp8.hip", "calibration.cpp")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(HERE, "libspectral.so")
 ARCH = "gfx950"

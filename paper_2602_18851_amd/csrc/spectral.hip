@@ -41,9 +41,13 @@
 #include <type_traits>
 #include <vector>
 
+#include "device_util.h"
+#include "logits_fp8.h"
 #include "spectral.h"
 
 namespace {
+
+using namespace sn_dev;
 
 thread_local std::string g_err;
 
@@ -67,7 +71,6 @@ constexpr int kMaxGC = 8;             // query heads per W_K work item
 constexpr int kQTargetItems = 16384;  // wave work items aimed for in a W_Q sweep
 constexpr int kKTargetItems = 4096;   // ... and in a W_K sweep (register-heavier waves)
 constexpr int kKMfmaResident = 3072;  // waves of the matrix-core W_K sweep resident at once (256 CUs x 12)
-constexpr int kRsrcWord3 = 0x00020000; // buffer descriptor word 3 for gfx9-family raw loads
 constexpr int kStreamPolicy = 2;       // cache policy of the weight loads: non-temporal (read once per sweep)
 
 // Sweep phases: the first W_K sweep from v, the W_Q and W_K sweeps of a step,
@@ -76,7 +79,7 @@ constexpr int kStreamPolicy = 2;       // cache policy of the weight loads: non-
 enum { PH_INIT = 0, PH_Q = 1, PH_K = 2, PH_EK = 3, PH_EQ = 4 };
 enum {
   KIND_INIT = 0, KIND_Q = 1, KIND_K = 2, KIND_FIN = 3, KIND_GRAM = 4, KIND_ITER = 5, KIND_EMIT = 6,
-  KIND_LROWS = 7, KIND_LCOLS = 8, KIND_LRED = 9, KIND_N = 10
+  KIND_LROWS = 7, KIND_LCOLS = 8, KIND_LRED = 9, KIND_PROJ = 10, KIND_LOGITS = 11, KIND_N = 12
 };
 static_assert(KIND_N == SN_PROFILE_KINDS, "profile kinds");
 
@@ -131,7 +134,6 @@ struct Traits<uint16_t> {  // bf16 bit patterns
   static constexpr int VEC = 8;
 };
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // one 16-byte chunk
 
 template <typename T>
 __device__ __forceinline__ float elem(const u32x4& q, int c);
@@ -174,21 +176,6 @@ __device__ __forceinline__ float group_sum(float x) {
   x += __shfl_xor(x, 16);
   x += __shfl_xor(x, 32);
   return x;
-}
-
-// Values that every lane of a wave computes identically (they come from the
-// same addresses) are moved to scalar registers explicitly: the compiler
-// cannot prove a load from writable memory wave-uniform, and a buffer
-// descriptor it believes divergent forces a loop around every buffer load.
-__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
-__device__ __forceinline__ float uni(float x) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, x)));
-}
-__device__ __forceinline__ const char* uni(const void* p) {
-  const uint64_t v = reinterpret_cast<uint64_t>(p);
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)v);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(v >> 32));
-  return reinterpret_cast<const char*>(((uint64_t)hi << 32) | lo);
 }
 
 // Work item of a sweep: which layer, which d_h-row block of that layer's
@@ -529,9 +516,7 @@ constexpr int kMTileC = 64;                // columns per tile: 128-byte row seg
 constexpr int kMPitch = kMTileC + 8;       // LDS row pitch of the K tile (144 B: 16-lane store passes conflict-free)
 constexpr int kMVPitch = kMTileC + 8;      // LDS row pitch of the split v'
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8 tr_read_8(const uint16_t* p0, const uint16_t* p1) {
   typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
@@ -1994,6 +1979,90 @@ SN_API int spectral_step_layer(sn_ctx* c, const void* const* wq_layers, const vo
   f.sigma = sigma;
   f.scale = scale;
   return timed(c, KIND_LRED, [&] { layer_finalize_kernel<<<dim3(L), kThreads, 0, c->stream>>>(f); });
+}
+
+SN_API int spectral_logits_workspace_bytes(const sn_shape* shape, int32_t seq_len, int64_t* bytes) {
+  if (!shape || !bytes) return fail(SN_ENULL, "shape and bytes must not be NULL");
+  if (seq_len < 1) return fail(SN_EINVAL, "seq_len must be >= 1");
+  *bytes = sn_logits_workspace_bytes(seq_len, (int64_t)shape->n_q_heads * shape->head_dim,
+                                     (int64_t)shape->n_kv_heads * shape->head_dim);
+  return SN_OK;
+}
+
+SN_API int spectral_logits_fp8(sn_ctx* c, const void* const* x_layers, int64_t ld_x, int32_t seq_len,
+                               const void* const* wq_layers, const void* const* wk_layers, const float* scale,
+                               void* workspace, int64_t workspace_bytes, uint8_t* codes, float* max_abs,
+                               int32_t* n_over) {
+  if (!c) return fail(SN_ENULL, "ctx must not be NULL");
+  if (!x_layers || !wq_layers || !wk_layers || !scale || !workspace || !max_abs || !n_over)
+    return fail(SN_ENULL, "x_layers, wq_layers, wk_layers, scale, workspace, max_abs and n_over must not be NULL");
+  const sn_shape& sh = c->shape;
+  if (sh.dtype != SN_BF16) return fail(SN_EDTYPE, "the logit consumer needs bf16 weights and tokens");
+  const int dh = sh.head_dim;
+  if (dh != 16 && dh != 32 && dh != 64 && dh != 128)
+    return fail(SN_EINVAL, "the logit consumer needs head_dim 16, 32, 64 or 128");
+  if (seq_len < 1 || seq_len > 46340) return fail(SN_EINVAL, "seq_len must be in [1, 46340]");
+  if (ld_x == 0) ld_x = sh.d_model;
+  if (ld_x < sh.d_model || (ld_x * 2) % 16 != 0) return fail(SN_EINVAL, "ld_x must be >= d_model, 8-element aligned");
+  const int64_t nq_cols = (int64_t)sh.n_q_heads * dh, nk_cols = (int64_t)sh.n_kv_heads * dh;
+  if ((int64_t)seq_len * ld_x * 2 >= (int64_t(1) << 31) || (int64_t)seq_len * nq_cols * 2 >= (int64_t(1) << 31))
+    return fail(SN_EINVAL, "seq_len x row bytes must stay below 2^31");
+  const int64_t need = sn_logits_workspace_bytes(seq_len, nq_cols, nk_cols);
+  if (workspace_bytes < need) return fail(SN_EINVAL, "workspace too small (spectral_logits_workspace_bytes)");
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) || (reinterpret_cast<uintptr_t>(codes) & 15))
+    return fail(SN_EINVAL, "workspace must be 256-byte and codes 16-byte aligned");
+  const int L = sh.n_layers;
+  for (int l = 0; l < L; ++l) {
+    if (!x_layers[l] || !wq_layers[l] || !wk_layers[l]) return fail(SN_ENULL, "a layer pointer is NULL");
+    if ((reinterpret_cast<uintptr_t>(x_layers[l]) | reinterpret_cast<uintptr_t>(wq_layers[l]) |
+         reinterpret_cast<uintptr_t>(wk_layers[l])) & 15)
+      return fail(SN_EINVAL, "layer pointers must be 16-byte aligned");
+  }
+  int cur_dev = 0;
+  SN_HIP(hipGetDevice(&cur_dev));
+  if (cur_dev != c->device) return fail(SN_ESTATE, "the current HIP device is not the context's device");
+
+  uint16_t* ws = reinterpret_cast<uint16_t*>(workspace);
+  ProjArgs p{};
+  p.ld_x = ld_x;
+  p.ld_w = sh.ld;
+  p.seq = seq_len;
+  p.d = sh.d_model;
+  p.nq_cols = (int32_t)nq_cols;
+  p.nk_cols = (int32_t)nk_cols;
+  p.tiles_m = ceil_div(seq_len, 128);
+  p.tiles_nq = ceil_div(nq_cols, 128);
+  p.tiles_nk = ceil_div(nk_cols, 128);
+  p.qh = ws;
+  p.ql = ws + (size_t)seq_len * nq_cols;
+  p.kh = ws + (size_t)2 * seq_len * nq_cols;
+  p.kl = p.kh + (size_t)seq_len * nk_cols;
+  LogitArgs g{};
+  g.qh = p.qh;
+  g.ql = p.ql;
+  g.kh = p.kh;
+  g.kl = p.kl;
+  g.seq = seq_len;
+  g.g = c->plan.g;
+  g.nq_cols = (int32_t)nq_cols;
+  g.nk_cols = (int32_t)nk_cols;
+  g.tiles = ceil_div(seq_len, 128);
+  g.scale = scale;
+  int rc = timed(c, KIND_LOGITS, [&] { sn_launch_zero_stats(max_abs, n_over, L * sh.n_q_heads, c->stream); });
+  if (rc != SN_OK) return rc;
+  for (int l = 0; l < L; ++l) {
+    p.x = reinterpret_cast<const uint16_t*>(x_layers[l]);
+    p.wq = reinterpret_cast<const uint16_t*>(wq_layers[l]);
+    p.wk = reinterpret_cast<const uint16_t*>(wk_layers[l]);
+    if ((rc = timed(c, KIND_PROJ, [&] { sn_launch_proj(p, c->stream); })) != SN_OK) return rc;
+    g.layer = l;
+    g.codes = codes ? codes + (size_t)l * sh.n_q_heads * seq_len * seq_len : nullptr;
+    g.max_abs = max_abs + (size_t)l * sh.n_q_heads;
+    g.n_over = n_over + (size_t)l * sh.n_q_heads;
+    if ((rc = timed(c, KIND_LOGITS, [&] { sn_launch_logits(g, dh, sh.n_q_heads, c->stream); })) != SN_OK)
+      return rc;
+  }
+  return SN_OK;
 }
 
 }  // extern "C"

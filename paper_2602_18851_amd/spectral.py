@@ -21,7 +21,7 @@ SN_FLAG_VALU_K_SWEEP = 1
 SN_FLAG_GRAM = 2
 SN_FLAG_LAYER = 4
 KIND_NAMES = ("k_sweep_first", "q_sweep", "k_sweep", "finalize", "gram_sweep", "gram_iterate", "gram_final_sweeps",
-              "layer_row_sweeps", "layer_col_sweeps", "layer_reduce")
+              "layer_row_sweeps", "layer_col_sweeps", "layer_reduce", "logits_projection", "logits_fp8")
 SN_PROFILE_KINDS = len(KIND_NAMES)
 
 EXPORTED = (
@@ -38,6 +38,8 @@ EXPORTED = (
     "spectral_overflow_terms",
     "spectral_auto_alpha",
     "spectral_slack_ratio",
+    "spectral_logits_workspace_bytes",
+    "spectral_logits_fp8",
 )
 
 
@@ -111,6 +113,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.spectral_auto_alpha.restype = ctypes.c_int
     lib.spectral_slack_ratio.argtypes = [ctypes.c_double, ctypes.c_double, i32, i32]
     lib.spectral_slack_ratio.restype = ctypes.c_double
+    lib.spectral_logits_workspace_bytes.argtypes = [ctypes.POINTER(sn_shape), i32, ctypes.POINTER(i64)]
+    lib.spectral_logits_workspace_bytes.restype = ctypes.c_int
+    lib.spectral_logits_fp8.argtypes = [vp, ctypes.POINTER(vp), i64, i32, ctypes.POINTER(vp), ctypes.POINTER(vp), vp,
+                                        vp, i64, vp, vp, vp]
+    lib.spectral_logits_fp8.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -207,6 +214,25 @@ def spectral_auto_alpha(slack: Sequence[float], quantile: float = 0.9999, kappa:
 
 def spectral_slack_ratio(max_abs_logit: float, sigma_layer: float, d_model: int, head_dim: int) -> float:
     return load_library().spectral_slack_ratio(max_abs_logit, sigma_layer, d_model, head_dim)
+
+
+def spectral_logits_workspace_bytes(shape: sn_shape, seq_len: int) -> int:
+    out = ctypes.c_int64(0)
+    _check(load_library().spectral_logits_workspace_bytes(ctypes.byref(shape), int(seq_len), ctypes.byref(out)))
+    return out.value
+
+
+def spectral_logits_fp8(ctx: int, x_ptrs: Sequence[int], ld_x: int, seq_len: int, wq_ptrs: Sequence[int],
+                        wk_ptrs: Sequence[int], scale: int, workspace: int, workspace_bytes: int, codes: int,
+                        max_abs: int, n_over: int) -> None:
+    n = len(wq_ptrs)
+    xs = (ctypes.c_void_p * n)(*x_ptrs)
+    wq = (ctypes.c_void_p * n)(*wq_ptrs)
+    wk = (ctypes.c_void_p * n)(*wk_ptrs)
+    _check(load_library().spectral_logits_fp8(ctypes.c_void_p(ctx), xs, int(ld_x), int(seq_len), wq, wk,
+                                              ctypes.c_void_p(scale), ctypes.c_void_p(workspace),
+                                              int(workspace_bytes), ctypes.c_void_p(codes or None),
+                                              ctypes.c_void_p(max_abs), ctypes.c_void_p(n_over)))
 
 
 # ----------------------------------------------------------- torch wrapper
@@ -317,6 +343,43 @@ class Spectral:
         spectral_step_layer(self.ctx, wq_p, wk_p, v.data_ptr(), u.data_ptr() if u is not None else 0, n_iter,
                             sigma.data_ptr(), scale.data_ptr())
         return sigma, scale
+
+    def logits_fp8(self, x, wq, wk, scale, want_codes: bool = False, workspace=None):
+        """FP8 E4M3 logit consumer.  x: bf16 [L, seq, d] tensor (or list of
+        [seq, >= d] row-major layers); scale: float32 [L] on the device.
+        Returns (max_abs [L, n_q], n_over [L, n_q], codes [L, n_q, seq, seq]
+        uint8 or None)."""
+        import torch
+
+        s = self.shape
+        L, nq = s.n_layers, s.n_q_heads
+        layers = list(x.unbind(0)) if isinstance(x, torch.Tensor) and x.dim() == 3 else list(x)
+        if len(layers) != L:
+            raise ValueError(f"expected {L} token layers, got {len(layers)}")
+        seq, ld_x = layers[0].shape[0], layers[0].stride(0)
+        for t in layers:
+            if not t.is_cuda or t.dtype != torch.bfloat16 or t.dim() != 2 or t.stride(1) != 1 \
+                    or t.shape[0] != seq or t.stride(0) != ld_x or t.shape[1] < s.d_model:
+                raise ValueError("token layers must be bf16 CUDA [seq, >= d] row-major with one row stride")
+        wq_p = self._layer_ptrs(wq, nq * s.head_dim)
+        wk_p = self._layer_ptrs(wk, s.n_kv_heads * s.head_dim)
+        if scale.dtype != torch.float32 or tuple(scale.shape) != (L,) or not scale.is_cuda:
+            raise ValueError(f"scale must be a float32 CUDA tensor of shape ({L},)")
+        dev = scale.device
+        need = spectral_logits_workspace_bytes(self.shape, seq)
+        if workspace is None or workspace.numel() < need:
+            workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+        max_abs = torch.empty(L, nq, dtype=torch.float32, device=dev)
+        n_over = torch.empty(L, nq, dtype=torch.int32, device=dev)
+        codes = torch.empty(L, nq, seq, seq, dtype=torch.uint8, device=dev) if want_codes else None
+        stream = torch.cuda.current_stream(dev).cuda_stream
+        if stream != self._stream:
+            spectral_set_stream(self.ctx, stream)
+            self._stream = stream
+        spectral_logits_fp8(self.ctx, [t.data_ptr() for t in layers], ld_x, seq, wq_p, wk_p, scale.data_ptr(),
+                            workspace.data_ptr(), workspace.numel(), codes.data_ptr() if want_codes else 0,
+                            max_abs.data_ptr(), n_over.data_ptr())
+        return max_abs, n_over, codes
 
     def profile(self, enable: bool = True):
         spectral_profile(self.ctx, enable)

@@ -1,0 +1,148 @@
+"""FP8 E4M3 logit consumer (spectral_logits_fp8) against the float64 oracle
+(oracle.fp8_consumer), through the C ABI.
+
+The GPU forms S~ = (q . k) / (sqrt(d_h) scale) from fp32 projections split
+into bf16 hi + lo halves (3 matrix-core products), so |S~_gpu - S~| stays
+below err_ij = 2^-14 ||q_i|| ||k_j|| / (sqrt(d_h) scale): the hi/lo split
+leaves at most 3 * 2^-16 of sum_r |q_r k_r| <= ||q|| ||k||, and the fp32
+sums of the projections add about sqrt(d) 2^-24 (~5e-6) relative.  Codes are
+unique away from the rounding points of E4M3; within err of one, either
+neighbour is correct.  So every GPU code must decode inside
+[dec(enc(S~ - err)), dec(enc(S~ + err))] (NaN allowed where that interval
+reaches past +-464), the overflow count must lie between the counts of
+|S~| > 448 + err and |S~| > 448 - err, and max |S~| must agree within the
+largest err."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import e4m3, fp8_consumer
+from workloads import WORKLOADS, all_weights, tokens
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # pragma: no cover - collected on CPU machines, skipped there
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2602_18851_amd import Spectral  # noqa: E402
+
+TAU = 2.0 ** -14
+
+
+def layer_tokens(wl, seq, layer):
+    """Post-normalisation tokens x = sqrt(d) u (Sec. 3.2), rounded to bf16."""
+    return torch.from_numpy(tokens(wl, seq, spherical=True, layer=layer)).to(torch.bfloat16)
+
+
+def _pad(t, ld):
+    if not ld or ld == t.shape[-1]:
+        return t.cuda()
+    p = torch.zeros(*t.shape[:-1], ld, dtype=t.dtype)
+    p[..., :t.shape[-1]] = t
+    return p.cuda()[..., :t.shape[-1]]
+
+
+def check_head(gpu_codes, gpu_max, gpu_over, x, wq, wk, scale, h, n_kv, dh):
+    x64 = x.double().numpy()
+    wq64, wk64 = wq.double().numpy(), wk.double().numpy()
+    S = fp8_consumer.head_logits(x64, wq64, wk64, h, n_kv, dh) / scale
+    g = (wq64.shape[0] // dh) // n_kv
+    qn = np.linalg.norm(x64 @ wq64[h * dh:(h + 1) * dh].T, axis=1)
+    kn = np.linalg.norm(x64 @ wk64[(h // g) * dh:(h // g + 1) * dh].T, axis=1)
+    err = TAU * np.outer(qn, kn) / (math.sqrt(dh) * scale)
+    # band of correct values; an end past -+464 is open (NaN codes there are correct too)
+    lo = np.where(S - err < -464.0, -np.inf, e4m3.decode(e4m3.encode(S - err)))
+    hi = np.where(S + err > 464.0, np.inf, e4m3.decode(e4m3.encode(S + err)))
+    got = e4m3.decode(gpu_codes)
+    with np.errstate(invalid="ignore"):
+        ok = np.isfinite(got) & (got >= lo) & (got <= hi)
+    ok |= np.isnan(got) & ((S + err > 464.0) | (S - err < -464.0))
+    assert ok.all(), (h, np.argwhere(~ok)[:5], S[~ok][:5], gpu_codes[~ok][:5])
+    exact = (e4m3.encode(S - err) == e4m3.encode(S + err))
+    assert (gpu_codes[exact] == e4m3.encode(S)[exact]).all()
+    a = np.abs(S)
+    assert np.count_nonzero(a > 448.0 + err) <= gpu_over <= np.count_nonzero(a > 448.0 - err)
+    assert abs(gpu_max - a.max()) <= err.max()
+    return int(np.count_nonzero(~exact)), float(a.max())
+
+
+CASES = [
+    # name, shape overrides, seq, ld (tokens and weights), target max |S~| per layer
+    ("gqa4-dh64-seq192", dict(n_layers=2, d_model=512, n_q=8, n_kv=2, head_dim=64), 192, 0, (540.0, 300.0)),
+    ("mha-dh128-ragged", dict(n_layers=1, d_model=1001, n_q=2, n_kv=2, head_dim=128), 130, 1008, (470.0,)),
+    ("mqa-dh16-seq64", dict(n_layers=1, d_model=256, n_q=8, n_kv=1, head_dim=16), 64, 0, (450.0,)),
+    ("gqa3-dh32-seq256", dict(n_layers=2, d_model=384, n_q=6, n_kv=2, head_dim=32), 256, 0, (1000.0, 100.0)),
+]
+
+
+@pytest.mark.parametrize("name,over,seq,ld,target", CASES, ids=[c[0] for c in CASES])
+def test_logits_against_oracle(name, over, seq, ld, target):
+    wl = WORKLOADS["llama2-70b-gqa"].replace(key=name, std=0.02, **over)
+    wq, wk = all_weights(wl, "cpu")
+    xs = [layer_tokens(wl, seq, l) for l in range(wl.n_layers)]
+    # scales chosen from the oracle's own logits so that the largest |S~| of
+    # every layer is the target (above 448: overflows and NaN codes)
+    scales = []
+    for l in range(wl.n_layers):
+        m = max(np.abs(fp8_consumer.head_logits(xs[l].double().numpy(), wq[l].double().numpy(),
+                                                wk[l].double().numpy(), h, wl.n_kv, wl.head_dim)).max()
+                for h in range(wl.n_q))
+        scales.append(m / target[l])
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, ld=ld)
+    x_dev = _pad(torch.stack(xs), ld)
+    scale_dev = torch.tensor(scales, dtype=torch.float32, device="cuda")
+    max_abs, n_over, codes = est.logits_fp8(x_dev, _pad(wq, ld), _pad(wk, ld), scale_dev, want_codes=True)
+    torch.cuda.synchronize()
+    max_abs, n_over, codes = max_abs.cpu().numpy(), n_over.cpu().numpy(), codes.cpu().numpy()
+    # the scale the GPU used is the float32 one
+    s32 = scale_dev.cpu().double().numpy()
+    band = 0
+    for l in range(wl.n_layers):
+        for h in range(wl.n_q):
+            nb, _ = check_head(codes[l, h], max_abs[l, h], n_over[l, h], xs[l], wq[l], wk[l], s32[l], h, wl.n_kv,
+                               wl.head_dim)
+            band += nb
+    assert n_over.sum() > 0
+    print(f"{name}: codes equal the oracle's outside the rounding bands ({band} entries inside one)")
+    # statistics without codes are the same
+    m2, o2, c2 = est.logits_fp8(x_dev, _pad(wq, ld), _pad(wk, ld), scale_dev, want_codes=False)
+    torch.cuda.synchronize()
+    assert c2 is None
+    np.testing.assert_array_equal(m2.cpu().numpy(), max_abs)
+    np.testing.assert_array_equal(o2.cpu().numpy(), n_over)
+    est.close()
+
+
+def test_zero_tokens_give_zero_logits():
+    wl = WORKLOADS["llama2-70b-gqa"].replace(n_layers=1, d_model=256, n_q=4, n_kv=2, head_dim=64)
+    gq, gk = all_weights(wl, "cuda")
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha)
+    x = torch.zeros(1, 100, wl.d_model, dtype=torch.bfloat16, device="cuda")
+    max_abs, n_over, codes = est.logits_fp8(x, gq, gk, torch.ones(1, device="cuda"), want_codes=True)
+    torch.cuda.synchronize()
+    assert not max_abs.any() and not n_over.any() and not codes.any()
+    est.close()
+
+
+def test_full_size_70b_sampled_heads():
+    """Llama-2-70B GQA shape, 1024 tokens per layer, all 80 layers on the GPU;
+    two heads of two layers against the oracle.  Per-layer scales are seeded
+    synthetic values around the size that puts the largest logit near 448."""
+    wl = WORKLOADS["llama2-70b-gqa"]
+    seq = 1024
+    gq, gk = all_weights(wl, "cuda")
+    x = torch.stack([layer_tokens(wl, seq, l) for l in range(wl.n_layers)]).cuda()
+    rng = np.random.default_rng(7)
+    scales = (0.02 * rng.uniform(0.5, 2.0, wl.n_layers)).astype(np.float32)
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha)
+    max_abs, n_over, codes = est.logits_fp8(x, gq, gk, torch.from_numpy(scales).cuda(), want_codes=True)
+    torch.cuda.synchronize()
+    for l, h in ((0, 0), (0, 37), (wl.n_layers - 1, 9), (wl.n_layers - 1, 63)):
+        check_head(codes[l, h].cpu().numpy(), max_abs[l, h].item(), n_over[l, h].item(), x[l].cpu(),
+                   gq[l].cpu(), gk[l].cpu(), float(scales[l]), h, wl.n_kv, wl.head_dim)
+    print(f"70B: max |S~| over all heads {max_abs.max().item():.1f}, overflowing heads "
+          f"{int((n_over > 0).sum())} of {n_over.numel()}")
+    est.close()

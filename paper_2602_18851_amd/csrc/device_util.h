@@ -35,4 +35,38 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRsrcWord3);
 }
 
+// ---- wave-private staging of row tiles through LDS ----------------------
+//
+// A tile is R rows x 128 bytes.  It is loaded with buffer_load ... lds, which
+// writes lane i's 16 bytes to LDS at base + 16 i: instruction j covers rows
+// 8 j .. 8 j + 7, eight consecutive lanes reading one 128-byte row segment
+// (a coalesced request for the address unit).  In LDS, row r holds its eight
+// 16-byte chunks at physical slot c ^ swz(r), swz(r) = (r / 2) mod 8, so a
+// 16-lane read of one chunk from rows r0 .. r0 + 15 (the MFMA operand
+// layout: lane s reads row r0 + s) touches 16 distinct bank groups.
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ int stage_swz(int r) { return (r >> 1) & 7; }
+
+// Issues the loads of one tile: row r of the resource starts at byte
+// r * row_bytes; the tile takes columns [col_byte, col_byte + 128).  AUX is the
+// cache policy of the loads.
+template <int R, int AUX>
+__device__ __forceinline__ void stage_issue(__amdgpu_buffer_rsrc_t rsrc, uint8_t* lds, uint32_t col_byte,
+                                            uint32_t row_bytes, int lane) {
+  const int sr = lane >> 3, p = lane & 7;
+#pragma unroll
+  for (int j = 0; j < R / 8; ++j) {
+    const int r = 8 * j + sr;
+    const uint32_t voff = (uint32_t)sr * row_bytes + col_byte + 16u * (uint32_t)(p ^ stage_swz(r));
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void*)(lds + 1024 * j), 16, voff, 8u * j * row_bytes, 0,
+                                             AUX);
+  }
+}
+
+// Logical 16-byte chunk c (0..7) of row r of a staged tile.
+__device__ __forceinline__ u32x4 stage_chunk(const uint8_t* lds, int r, int c) {
+  return *reinterpret_cast<const u32x4*>(lds + 128 * r + 16 * (c ^ stage_swz(r)));
+}
+
 }  // namespace sn_dev

@@ -30,7 +30,6 @@ using namespace sn_dev;
 
 constexpr int kWaves = 4;      // 2 x 2 waves of 64 x 64 per 128 x 128 workgroup tile
 constexpr int kTile = 128;
-constexpr int kLdsPitch = 68;  // bytes per row of a wave's 64 x 64 code tile in LDS
 
 __device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, const f32x4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
@@ -48,55 +47,69 @@ __device__ __forceinline__ uint16_t bf16_bits(float x) { return __builtin_bit_ca
 
 // Q and K projections of one layer.  Tiles of 128 tokens x 128 output
 // features, Q features first, then K; a wave covers 64 x 64 (4 x 4 blocks of
-// 16 x 16).  Operands come straight from memory in the MFMA layout (lane l:
-// row l % 16, 16 bytes of consecutive k at 8 (l / 16)); two loads per 16-row
-// block cover one 128-byte segment of each row.  Workgroups are numbered so
-// that the consecutive token tiles of one feature tile run on one XCD (the
-// hardware deals workgroups round-robin over the 8 XCDs) and share its L2.
+// 16 x 16).  The workgroup streams the 128 token rows and 128 weight rows of
+// its tile through LDS in steps of 64 columns (128-byte row segments, coalesced
+// loads straight to LDS, two stages; see stage_issue), and every wave reads
+// its operands back in the MFMA layout.  Workgroups are numbered so that the
+// consecutive token tiles of one feature tile run on one XCD (the hardware
+// deals workgroups round-robin over the 8 XCDs) and share its L2.
+constexpr int kStageBytes = 2 * kTile * 128;  // A and B rows of one 64-column step
+
 __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t stage[2][kStageBytes];
   const int lane = threadIdx.x & 63;
   const int wv = uni((int)(threadIdx.x >> 6));
   const int q = lane >> 4, s = lane & 15;
   const int per_xcd = gridDim.x / 8;
   const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   const int tiles_q = a.tiles_m * a.tiles_nq;
-  if (t >= tiles_q + a.tiles_m * a.tiles_nk) return;
+  if (t >= tiles_q + a.tiles_m * a.tiles_nk) return;  // whole workgroup
   const bool isq = t < tiles_q;
   const int tt = isq ? t : t - tiles_q;
   const int bm = tt % a.tiles_m, bn = tt / a.tiles_m;
   const int ncols = isq ? a.nq_cols : a.nk_cols;
-  const int m0 = bm * kTile + (wv >> 1) * 64, n0 = bn * kTile + (wv & 1) * 64;
-  if (m0 >= a.seq || n0 >= ncols) return;
 
-  const char* abase = reinterpret_cast<const char*>(a.x) + (int64_t)m0 * a.ld_x * 2;
-  const char* bbase = reinterpret_cast<const char*>(isq ? a.wq : a.wk) + (int64_t)n0 * a.ld_w * 2;
-  const __amdgpu_buffer_rsrc_t ra =
-      make_rsrc(abase, (uint32_t)((((int64_t)(a.seq - 1 - m0) * a.ld_x + a.d) * 2 + 15) & ~int64_t(15)));
-  const __amdgpu_buffer_rsrc_t rb_ =
-      make_rsrc(bbase, (uint32_t)((((int64_t)(ncols - 1 - n0) * a.ld_w + a.d) * 2 + 15) & ~int64_t(15)));
-  const uint32_t a_off = (uint32_t)(s * a.ld_x * 2 + 16 * q), b_off = (uint32_t)(s * a.ld_w * 2 + 16 * q);
-  const uint32_t a_row16 = (uint32_t)(16 * a.ld_x * 2), b_row16 = (uint32_t)(16 * a.ld_w * 2);
+  // this wave stages rows 32 wv .. 32 wv + 31 of the A (token) and B (weight) tiles
+  const int am = bm * kTile + 32 * wv, bnr = bn * kTile + 32 * wv;
+  const char* abase = reinterpret_cast<const char*>(a.x) + (int64_t)am * a.ld_x * 2;
+  const char* bbase = reinterpret_cast<const char*>(isq ? a.wq : a.wk) + (int64_t)bnr * a.ld_w * 2;
+  const int64_t a_len = am < a.seq ? (((int64_t)(a.seq - 1 - am) * a.ld_x + a.d) * 2 + 15) & ~int64_t(15) : 0;
+  const int64_t b_len = bnr < ncols ? (((int64_t)(ncols - 1 - bnr) * a.ld_w + a.d) * 2 + 15) & ~int64_t(15) : 0;
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(abase, (uint32_t)a_len);
+  const __amdgpu_buffer_rsrc_t rb_ = make_rsrc(bbase, (uint32_t)b_len);
+  const uint32_t a_rb = (uint32_t)(a.ld_x * 2), b_rb = (uint32_t)(a.ld_w * 2);
+  auto issue = [&](int k, int st) {
+    stage_issue<32, 0>(ra, stage[st] + 4096 * wv, (uint32_t)(k * 128), a_rb, lane);
+    stage_issue<32, 0>(rb_, stage[st] + kTile * 128 + 4096 * wv, (uint32_t)(k * 128), b_rb, lane);
+  };
 
+  const int wm = wv >> 1, wn = wv & 1;
   f32x4 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int n_kt = (a.d + 63) / 64, n_full = a.d / 64;
+  const int n_k = (a.d + 63) / 64, n_full = a.d / 64;
+  issue(0, 0);
 #pragma unroll 1
-  for (int kt = 0; kt < n_kt; ++kt) {
+  for (int k = 0; k < n_k; ++k) {
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's part of step k is in LDS
+    __syncthreads();                // every part, and step k - 1 fully read
+    if (k + 1 < n_k) issue(k + 1, (k + 1) & 1);
+    const uint8_t* sa = stage[k & 1];
+    const uint8_t* sb = sa + kTile * 128;
     u32x4 fa[4][2], fb[4][2];
 #pragma unroll
     for (int r = 0; r < 4; ++r)
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc) {
-        fa[r][kc] = __builtin_amdgcn_raw_buffer_load_b128(ra, a_off + kt * 128 + 64 * kc, r * a_row16, 0);
-        fb[r][kc] = __builtin_amdgcn_raw_buffer_load_b128(rb_, b_off + kt * 128 + 64 * kc, r * b_row16, 0);
+        fa[r][kc] = stage_chunk(sa, 64 * wm + 16 * r + s, 4 * kc + q);
+        fb[r][kc] = stage_chunk(sb, 64 * wn + 16 * r + s, 4 * kc + q);
       }
-    if (kt >= n_full) {  // the ragged last k tile: zero columns >= d
+    if (k >= n_full) {  // the ragged last step: zero columns >= d
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc) {
-        const int nval = a.d - (kt * 64 + 32 * kc + 8 * q);
+        const int nval = a.d - (k * 64 + 32 * kc + 8 * q);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           mask_bf16(fa[r][kc], nval);
@@ -112,6 +125,7 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs a) {
         for (int j = 0; j < 4; ++j) acc[i][j] = mfma(fa[i][kc], fb[j][kc], acc[i][j]);
   }
 
+  const int m0 = bm * kTile + 64 * wm, n0 = bn * kTile + 64 * wn;
   uint16_t* hi = isq ? a.qh : a.kh;
   uint16_t* lo = isq ? a.ql : a.kl;
 #pragma unroll
@@ -130,34 +144,18 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs a) {
       }
 }
 
-// OCP E4M3FN code of an fp32 value, round to nearest even: magnitudes in
-// [448, 464] give 448 (464 is the tie between 448 and the absent 480, and
-// 448's mantissa is even), larger ones and NaN give the NaN code 0x7F.
-__device__ __forceinline__ uint32_t e4m3_code(float x) {
-  const uint32_t b = __float_as_uint(x);
-  const uint32_t sign = (b >> 24) & 0x80u;
-  const float ax = fabsf(x);
-  if (!(ax <= 464.f)) return sign | 0x7Fu;
-  if (ax >= 448.f) return sign | 0x7Eu;
-  if (ax < 0.015625f) return sign | (uint32_t)__builtin_rintf(ax * 512.f);  // m * 2^-9, m = 0..8
-  const uint32_t ab = b & 0x7FFFFFFFu;
-  int e = (int)(ab >> 23) - 127;  // -6 .. 8
-  uint32_t man = (ab >> 20) & 7u;
-  const uint32_t rem = ab & 0xFFFFFu;
-  if (rem > 0x80000u || (rem == 0x80000u && (man & 1u))) ++man;
-  if (man == 8u) {
-    man = 0u;
-    ++e;
-  }
-  return sign | ((uint32_t)(e + 7) << 3) | man;
-}
-
 // Logits of one layer: one 128 x 128 tile of S for one query head per
-// workgroup, 64 x 64 per wave, K-dimension d_h in steps of 32.
+// workgroup, 64 x 64 per wave, contraction over d_h in steps of 32.  The
+// products are formed transposed (A = key rows, B = query rows), so a lane
+// holds 4 consecutive columns of one row of S: one 32-bit word of E4M3
+// codes.  v_cvt_pk_fp8_f32 (no clamp) rounds to nearest even and gives the
+// NaN code past 464, the OCP E4M3FN conversion the oracle defines; a
+// bit-by-bit comparison with an integer encoder over every rounding point
+// and 400k random values in [-600, 600] found no difference for non-NaN
+// inputs.
 template <int DH>
 __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
   constexpr int KC = (DH + 31) / 32;
-  __shared__ __attribute__((aligned(16))) uint8_t lds[kWaves][64 * kLdsPitch];
   const int lane = threadIdx.x & 63;
   const int wv = uni((int)(threadIdx.x >> 6));
   const int q = lane >> 4, s = lane & 15;
@@ -177,7 +175,7 @@ __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
   const uint32_t q_off = (uint32_t)(s * qrow + 16 * q), k_off = (uint32_t)(s * krow + 16 * q);
   const uint32_t q16 = (uint32_t)(16 * qrow), k16 = (uint32_t)(16 * krow);
 
-  f32x4 acc[4][4];
+  f32x4 acc[4][4];  // acc[i][j][e] = S[i0 + 16 i + s][j0 + 16 j + 4 q + e]
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -198,52 +196,43 @@ __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        acc[i][j] = mfma(ah[i], bh[j], acc[i][j]);
-        acc[i][j] = mfma(ah[i], bl[j], acc[i][j]);
-        acc[i][j] = mfma(al[i], bh[j], acc[i][j]);
+        acc[i][j] = mfma(bh[j], ah[i], acc[i][j]);
+        acc[i][j] = mfma(bl[j], ah[i], acc[i][j]);
+        acc[i][j] = mfma(bh[j], al[i], acc[i][j]);
       }
   }
 
   // S~ = (q . k) / (sqrt(d_h) scale), the factor formed in double
   const float c = (float)(1.0 / (std::sqrt((double)DH) * (double)a.scale[a.layer]));
-  uint8_t* tile = lds[wv];
+  const bool words = (a.seq & 3) == 0;  // rows start 4-byte aligned
   int n_over = 0;
   float mx = 0.f;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 4; ++i) {
+    const int row = i0 + 16 * i + s;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 4; ++j) {
+      const int col = j0 + 16 * j + 4 * q;
+      float v[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int r = 16 * i + 4 * q + e, col = 16 * j + s;
-        const bool in = (i0 + r < a.seq) && (j0 + col < a.seq);
-        const float v = acc[i][j][e] * c;
-        const float av = fabsf(v);
+        v[e] = acc[i][j][e] * c;
+        const bool in = row < a.seq && col + e < a.seq;
+        const float av = fabsf(v[e]);
         n_over += (in && av > 448.f) ? 1 : 0;
         mx = in ? fmaxf(mx, av) : mx;
-        tile[r * kLdsPitch + col] = (uint8_t)e4m3_code(v);
       }
-  if (a.codes) {
-    // lane = row of the tile: 64 bytes out, whole 16-byte stores where the
-    // row lies inside the matrix
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    const int row = i0 + lane;
-    if (row < a.seq) {
-      uint8_t* out = a.codes + ((size_t)h * a.seq + row) * a.seq + j0;
-      const uint8_t* src = tile + lane * kLdsPitch;
-      const int ncol = min(64, a.seq - j0);
-      if (ncol == 64 && (a.seq & 15) == 0) {
+      if (a.codes && row < a.seq) {
+        int w = __builtin_amdgcn_cvt_pk_fp8_f32(v[0], v[1], 0, false);
+        w = __builtin_amdgcn_cvt_pk_fp8_f32(v[2], v[3], w, true);
+        uint8_t* out = a.codes + ((size_t)h * a.seq + row) * a.seq + col;
+        if (words && col + 3 < a.seq) {
+          *reinterpret_cast<int*>(out) = w;
+        } else {
 #pragma unroll
-        for (int c16 = 0; c16 < 4; ++c16) {
-          u32x4 w;
-#pragma unroll
-          for (int b = 0; b < 4; ++b) w[b] = *reinterpret_cast<const uint32_t*>(src + 16 * c16 + 4 * b);
-          *reinterpret_cast<u32x4*>(out + 16 * c16) = w;
+          for (int e = 0; e < 4; ++e)
+            if (col + e < a.seq) out[e] = (uint8_t)(w >> (8 * e));
         }
-      } else {
-        for (int cc = 0; cc < ncol; ++cc) out[cc] = src[cc];
       }
     }
   }

@@ -745,8 +745,9 @@ ksweep_mfma_kernel(SweepArgs a) {
 // operand is rows 16 bj.. of R, both in the rows' native layout (lane l
 // holds row l % 16 and 16 bytes of consecutive columns; the contraction
 // index may be permuted freely as long as both operands share it).  Only the
-// upper triangle of blocks is formed.  Two loads per 16-row block cover one
-// 128-byte segment of each row, back to back.
+// upper triangle of blocks is formed.  A wave streams its rows through LDS in
+// tiles of 128-byte row segments (coalesced loads; see stage_issue) and reads
+// the operands back in the MFMA layout.
 constexpr int kGWaves = 4;                 // waves per workgroup of the Gram sweep
 constexpr int kGTargetItems = 4096;        // Gram work items aimed for (about two waves per SIMD)
 
@@ -770,6 +771,7 @@ gram_kernel(GramArgs a) {
   constexpr int RB = DH / 16;
   constexpr int NB = RB * (RB + 1) / 2;
   constexpr int TC = 128 / ES;  // columns per tile
+  __shared__ __attribute__((aligned(16))) uint8_t stage[kGWaves][DH * 128];
   const int lane = threadIdx.x & 63;
   const int wv = uni((int)(threadIdx.x >> 6));
   const int q = lane >> 4, s = lane & 15;
@@ -790,8 +792,8 @@ gram_kernel(GramArgs a) {
   const uint32_t nrec = (uint32_t)((((int64_t)(DH - 1) * a.ld + a.d) * ES + 15) & ~int64_t(15));
   const __amdgpu_buffer_rsrc_t rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(blk), (short)0, (int)nrec, kRsrcWord3);
-  const uint32_t lane_off = (uint32_t)((int64_t)s * a.ld * ES + 16 * q);
   const uint32_t row_bytes = (uint32_t)(a.ld * ES);
+  uint8_t* tile = stage[wv];
 
   f32x4 acc[NB];
 #pragma unroll
@@ -800,15 +802,19 @@ gram_kernel(GramArgs a) {
   const int t0 = strip * a.tps;
   const int t1 = min(t0 + a.tps, a.n_tiles);
 
+  // one LDS tile per wave: tile t + 1 streams in while tile t is multiplied
+  // from registers
+  if (t0 < t1) stage_issue<DH, kStreamPolicy>(rsrc, tile, (uint32_t)(t0 * 128), row_bytes, lane);
 #pragma unroll 1
   for (int t = t0; t < t1; ++t) {
+    __builtin_amdgcn_s_waitcnt(0);  // the tile is in LDS
     u32x4 fr[RB][2];
-    const uint32_t voff = lane_off + (uint32_t)(t * 128);
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-      for (int kc = 0; kc < 2; ++kc)
-        fr[rb][kc] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff + 64 * kc, 16 * rb * row_bytes, kStreamPolicy);
+      for (int kc = 0; kc < 2; ++kc) fr[rb][kc] = stage_chunk(tile, 16 * rb + s, 4 * kc + q);
+    __builtin_amdgcn_s_waitcnt(0);  // read out before the next tile overwrites it
+    if (t + 1 < t1) stage_issue<DH, kStreamPolicy>(rsrc, tile, (uint32_t)((t + 1) * 128), row_bytes, lane);
     if (t >= n_full) {  // the ragged last tile: zero columns >= d
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc) {

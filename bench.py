@@ -45,9 +45,11 @@ def parse():
     p.add_argument("--q-strips", type=int, default=0, help="column strips per head in the W_Q sweep (0 = auto)")
     p.add_argument("--k-strips", type=int, default=0, help="column strips per KV head in the W_K sweep (0 = auto)")
     p.add_argument("--flags", type=int, default=0, help="sn_params.flags (SN_FLAG_* bits)")
-    p.add_argument("--form", choices=("chain", "gram", "layer"), default="chain",
+    p.add_argument("--form", choices=("chain", "gram", "layer", "fp8"), default="chain",
                    help="gram: the Gram form of the iteration (adds SN_FLAG_GRAM); layer: the paper-literal "
-                        "layer-level estimator (one u, v per layer, spectral_step_layer)")
+                        "layer-level estimator (one u, v per layer, spectral_step_layer); fp8: the E4M3 logit "
+                        "consumer of the scale (spectral_logits_fp8) on --seq tokens per layer")
+    p.add_argument("--seq", type=int, default=1024, help="tokens per layer of the fp8 form")
     p.add_argument("--mode", choices=("bench", "copy"), default="bench",
                    help="copy: one plain device copy of --copy-bytes, the reference for HBM byte counters")
     p.add_argument("--copy-bytes", type=int, default=4 << 30)
@@ -72,9 +74,10 @@ def source_hash() -> str:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def measured_traffic(n_layers_bytes: float):
-    """HBM bytes per W_Q-sweep launch from the committed rocprofv3 counter
-    summary, if it was taken on the current kernel source; else None."""
+def measured_traffic(kernel: str = ""):
+    """HBM bytes per launch of the W_Q sweep (or of ``kernel``, a sub-entry
+    such as "gram_sweep") from the committed rocprofv3 counter summary, if it
+    was taken on the current kernel source; else None."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
@@ -82,7 +85,7 @@ def measured_traffic(n_layers_bytes: float):
         return None
     if t.get("source_sha256_16") != source_hash():
         return None
-    return t.get("bytes_per_launch")
+    return (t.get(kernel) or {}).get("bytes_per_launch") if kernel else t.get("bytes_per_launch")
 
 
 def cpu_baseline(wl, budget_s: float, n_iter: int):
@@ -116,6 +119,132 @@ def cpu_baseline(wl, budget_s: float, n_iter: int):
     }
 
 
+def cpu_baseline_layer(wl, budget_s: float, n_iter: int):
+    """The oracle's paper-literal layer estimator on host cores, layer 0 repeated."""
+    from threadpoolctl import threadpool_info
+
+    from oracle.power_iteration import power_iteration_layer
+    from workloads import layer_start_vectors, layer_weights
+
+    v0 = layer_start_vectors(wl.replace(n_layers=1), "cpu")[0].double().numpy()
+    wq, wk = layer_weights(wl, 0, "cpu")
+    wq, wk = wq.double().numpy().T, wk.double().numpy().T
+    runs = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < budget_s:
+        power_iteration_layer(wq, wk, v0, n_iter, wl.n_q // wl.n_kv, wl.head_dim)
+        runs += 1
+    dt = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": runs * n_iter / dt, "unit": "layers·iters/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{runs} runs of the layer-0 estimator, {n_iter} iterations each, float64 numpy, {dt:.1f} s"}
+
+
+def cpu_baseline_fp8(wl, budget_s: float, seq: int):
+    """The oracle's E4M3 logit consumer on host cores: heads of layer 0 in turn."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    from oracle import fp8_consumer
+    from workloads import layer_weights, tokens
+
+    wq, wk = layer_weights(wl, 0, "cpu")
+    wq, wk = wq.double().numpy(), wk.double().numpy()
+    x = torch.from_numpy(tokens(wl, seq, spherical=True, layer=0)).to(torch.bfloat16).double().numpy()
+    heads = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < budget_s:
+        fp8_consumer.consume_layer(x, wq, wk, 0.05, wl.n_kv, wl.head_dim, heads=[heads % wl.n_q])
+        heads += 1
+    dt = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": heads * seq * seq / dt, "unit": "scaled logits/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{heads} heads of layer 0 ({seq} tokens: projections, logits, E4M3 codes, counts), "
+                      f"float64 numpy, {dt:.1f} s"}
+
+
+def bench_fp8(args):
+    """The E4M3 logit consumer: every layer and query head of the workload on
+    --seq post-normalisation tokens per layer, codes written."""
+    import numpy as np
+    import torch
+
+    from paper_2602_18851_amd import Spectral
+    from paper_2602_18851_amd.spectral import SN_FLAG_GRAM
+    from workloads import WORKLOADS, all_weights, start_vectors, tokens
+
+    wl = WORKLOADS[args.workload]
+    seq = args.seq
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    wq, wk = all_weights(wl, dev)
+    x = torch.stack([torch.from_numpy(tokens(wl, seq, spherical=True, layer=l)).to(torch.bfloat16)
+                     for l in range(wl.n_layers)]).to(dev)
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, flags=SN_FLAG_GRAM)
+    _, scale, _ = est.step(wq, wk, start_vectors(wl, dev), wl.n_iter)   # the layer scales the consumer uses
+    ws = torch.empty(seq * (wl.n_q + wl.n_kv) * wl.head_dim * 4, dtype=torch.uint8, device=dev)
+    codes = torch.empty(wl.n_layers, wl.n_q, seq, seq, dtype=torch.uint8, device=dev)
+
+    # the timed call writes the codes; buffers are allocated once, outside it
+    from paper_2602_18851_amd.spectral import spectral_logits_fp8
+    max_abs = torch.empty(wl.n_layers, wl.n_q, dtype=torch.float32, device=dev)
+    n_over = torch.empty(wl.n_layers, wl.n_q, dtype=torch.int32, device=dev)
+    xs = [t.data_ptr() for t in x.unbind(0)]
+    wqs = [t.data_ptr() for t in wq.unbind(0)]
+    wks = [t.data_ptr() for t in wk.unbind(0)]
+
+    def step():
+        spectral_logits_fp8(est.ctx, xs, wl.d_model, seq, wqs, wks, scale.data_ptr(), ws.data_ptr(), ws.numel(),
+                            codes.data_ptr(), max_abs.data_ptr(), n_over.data_ptr())
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall_s = time.perf_counter() - t_wall
+    ms = e0.elapsed_time(e1) / args.steps
+    est.profile(True)
+    step()
+    prof = est.profile_read()
+    est.profile(False)
+    p_ms, p_n = prof["logits_projection"]
+    l_ms, l_n = prof["logits_fp8"]
+    proj_flops = 2.0 * seq * wl.d_model * (wl.n_q + wl.n_kv) * wl.head_dim   # per launch (one layer)
+    logit_flops = 3 * 2.0 * seq * seq * wl.head_dim * wl.n_q                  # per launch, three bf16 products
+    tflops = proj_flops / (p_ms / p_n * 1e-3) / 1e12
+    logits = wl.n_layers * wl.n_q * seq * seq
+    out = {
+        "metric": "scaled E4M3 attention logits/sec (all layers and query heads)",
+        "value": logits / (ms * 1e-3), "unit": "logits/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.key + "-fp8-consumer", "n_layers": wl.n_layers, "d_model": wl.d_model,
+                   "n_q_heads": wl.n_q, "n_kv_heads": wl.n_kv, "head_dim": wl.head_dim, "seq_len": seq,
+                   "tokens": "x = sqrt(d) u, u uniform on the sphere, per layer, bf16",
+                   "scale": f"Eq. scale from the estimator, alpha {wl.alpha}", "form": "fp8"},
+        "wall_s_timed": wall_s,
+        "kernels_ms_per_step": {k: t for k, (t, n) in prof.items() if n},
+        "max_abs_scaled": float(max_abs.max()), "overflow_heads": int((n_over > 0).sum()),
+        "roofline": {
+            "kernel": "logits_projection (Q, K = X W^T, bf16 matrix cores)",
+            "bound": "mfma", "achieved": tflops, "peak": 2500.0, "unit": "TFLOP/s", "frac": tflops / 2500.0,
+            "traffic": None, "algorithmic_flops_per_launch": proj_flops, "avg_launch_ms": p_ms / p_n,
+            "launches": p_n,
+            "logits_kernel_TFLOPs": logit_flops / (l_ms / max(l_n - 1, 1) * 1e-3) / 1e12,
+        },
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_fp8(wl, args.cpu_seconds, seq)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -123,6 +252,9 @@ def main():
         sys.exit(2)
     if args.mode == "copy":
         copy_reference(args.copy_bytes)
+        return
+    if args.form == "fp8":
+        bench_fp8(args)
         return
 
     import torch
@@ -247,7 +379,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": None if (gram or layer) else measured_traffic(dom_alg),
+            "traffic": None if layer else measured_traffic("gram_sweep" if gram else ""),
             "algorithmic_bytes_per_launch": dom_alg,
             "avg_launch_ms": dom_avg_ms,
             "launches": dom_n,
@@ -258,7 +390,7 @@ def main():
         out["roofline"]["mfma_frac_of_dense_peak"] = out["roofline"]["mfma_TFLOPs"] / (2500.0 if wl.dtype == "bf16"
                                                                                         else 157.3)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, n_iter)
+        out["cpu_baseline"] = (cpu_baseline_layer if layer else cpu_baseline)(wl, args.cpu_seconds, n_iter)
     print(json.dumps(out), flush=True)
 
 

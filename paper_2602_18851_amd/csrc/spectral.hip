@@ -70,7 +70,7 @@ constexpr int kCPL = 8;               // 16-byte column chunks per wave row (lan
 constexpr int kMaxGC = 8;             // query heads per W_K work item
 constexpr int kQTargetItems = 16384;  // wave work items aimed for in a W_Q sweep
 constexpr int kKTargetItems = 4096;   // ... and in a W_K sweep (register-heavier waves)
-constexpr int kKMfmaResident = 3072;  // waves of the matrix-core W_K sweep resident at once (256 CUs x 12)
+constexpr int kKMfmaResident = 2048;  // waves of the matrix-core W_K sweep resident at once (256 CUs x 8)
 constexpr int kStreamPolicy = 2;       // cache policy of the weight loads: non-temporal (read once per sweep)
 
 // Sweep phases: the first W_K sweep from v, the W_Q and W_K sweeps of a step,
@@ -499,30 +499,33 @@ sweep_kernel(SweepArgs a) {
 // fp32 vector is split as x = hi + lo into two bf16 values (|x - hi - lo| <=
 // 2^-16 |x|) so the products keep ~16 significant bits while K stays in its
 // native bf16.
-//   Product 2 (contraction over columns) takes K straight from the registers
-//   it was loaded into: lane = 16 * g + s holds row s of a 16-row block and 8
-//   consecutive columns, which is the MFMA A-operand layout.
-//   Product 1 (contraction over rows) needs column fragments: the tile is
-//   written to LDS row-major and read back with ds_read_b64_tr_b16, which
-//   within each 16-lane group hands lane t element (t % 4) of source lane
-//   4j + t / 4 for j = 0..3; pointing source lane s at row k0 + s / 4,
-//   column 4 (s % 4) gives lane t rows k0 .. k0 + 3 of column t.
+//   Each tile (d_h rows x 64 columns of K_j) is staged once in LDS by
+//   coalesced loads (stage_issue) and read twice from there:
+//   Product 1 (contraction over rows) needs column fragments, read with
+//   ds_read_b64_tr_b16, which within each 16-lane group hands lane t element
+//   (t % 4) of source lane 4j + t / 4 for j = 0..3; pointing source lane s at
+//   row k0 + s / 4, column 4 (s % 4) gives lane t rows k0 .. k0 + 3 of
+//   column t.
+//   Product 2 (contraction over columns) reads the A-operand layout: lane
+//   16 g + s holds row s of a 16-row block and 8 consecutive columns.
 //   v' (16 slots x 64 columns) goes back through LDS to reach the B-operand
 //   layout of product 2.
-// The tile goes through LDS in two 64-row halves, which keeps a 2-wave
-// workgroup at 23 KB of LDS and 12 waves per CU in flight.
+// The loads of tile t + 1 are in flight while tile t is multiplied.
 constexpr int kMWaves = 2;                 // waves per workgroup
-constexpr int kMTileC = 64;                // columns per tile: 128-byte row segments per load
-constexpr int kMPitch = kMTileC + 8;       // LDS row pitch of the K tile (144 B: 16-lane store passes conflict-free)
+constexpr int kMTileC = 64;                // columns per tile: 128-byte row segments
 constexpr int kMVPitch = kMTileC + 8;      // LDS row pitch of the split v'
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ bf16x8 tr_read_8(const uint16_t* p0, const uint16_t* p1) {
+// Rows r and r + 4 of a staged tile, columns col .. col + 3, transposed over
+// each 16-lane group (see the comment above).
+__device__ __forceinline__ bf16x8 tr_read_staged(const uint8_t* tile, int r, int col) {
   typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-  const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p0));
-  const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p1));
-  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7));
+  const uint8_t* p0 = tile + 128 * r + 16 * ((col >> 3) ^ stage_swz(r)) + 2 * (col & 7);
+  const uint8_t* p1 = tile + 128 * (r + 4) + 16 * ((col >> 3) ^ stage_swz(r + 4)) + 2 * (col & 7);
+  const s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p0));
+  const s16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p1));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 template <int GC>
@@ -534,7 +537,7 @@ __device__ __forceinline__ bool pick(const bool (&f)[GC], int i) {
 }
 
 template <int DH, int PH>
-__global__ void __launch_bounds__(64 * kMWaves) __attribute__((amdgpu_waves_per_eu(3)))
+__global__ void __launch_bounds__(64 * kMWaves) __attribute__((amdgpu_waves_per_eu(2)))
 ksweep_mfma_kernel(SweepArgs a) {
   constexpr int GC = 8;
   constexpr int RB = DH / 16;          // 16-row blocks (product-2 M blocks)
@@ -542,10 +545,8 @@ ksweep_mfma_kernel(SweepArgs a) {
   constexpr int CB = kMTileC / 16;     // 16-column blocks (product-1 N blocks)
   constexpr int KC = kMTileC / 32;     // 32-column blocks (product-2 K blocks)
   constexpr int ES = 2;
-  constexpr int SR = DH < 64 ? DH : 64;  // rows staged in LDS at a time (product 1 runs per half)
-  constexpr int NHALF = DH / SR;
-  static_assert(SR * kMPitch * 2 >= GC * DH * 4, "input vectors alias the tile buffer");
-  __shared__ __attribute__((aligned(16))) uint16_t lds_tile[kMWaves][SR * kMPitch];
+  static_assert(DH * 128 >= GC * DH * 4, "input vectors alias the tile buffer");
+  __shared__ __attribute__((aligned(16))) uint8_t lds_tile[kMWaves][DH * 128];
   __shared__ __attribute__((aligned(16))) uint16_t lds_v[kMWaves][16 * kMVPitch];
 
   const int lane = threadIdx.x & 63;
@@ -554,7 +555,8 @@ ksweep_mfma_kernel(SweepArgs a) {
   const Item itm = decode_item<DH, GC, PH>(a, blockIdx.x * kMWaves + wv);
   const int head0 = itm.head0, strip = itm.strip;
   const int slot_cur = a.k & 1;
-  float (*xs)[DH] = reinterpret_cast<float (*)[DH]>(&lds_tile[wv][0]);  // only until the first tile
+  uint8_t* tl = &lds_tile[wv][0];
+  float (*xs)[DH] = reinterpret_cast<float (*)[DH]>(tl);  // only until the first tile is staged
   bool act[GC], last[GC];
   head_setup<DH, GC, PH>(a, itm, lane, xs, act, last);
   __syncthreads();
@@ -586,20 +588,8 @@ ksweep_mfma_kernel(SweepArgs a) {
 
   const char* blk = uni(a.mats[itm.layer]) + (int64_t)itm.row0 * a.ld * ES;
   const uint32_t nrec = (uint32_t)((((int64_t)(DH - 1) * a.ld + a.d) * ES + 15) & ~int64_t(15));
-  const __amdgpu_buffer_rsrc_t rsrc =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(blk), (short)0, (int)nrec, kRsrcWord3);
-  const uint32_t lane_off = (uint32_t)(((int64_t)s * a.ld + 8 * g) * ES);
+  const __amdgpu_buffer_rsrc_t rsrc = make_rsrc(blk, nrec);
   const uint32_t row_bytes = (uint32_t)(a.ld * ES);
-
-  auto load_tile = [&](u32x4 (&buf)[RB][KC], int t) {
-    const uint32_t voff = lane_off + (uint32_t)(t * kMTileC * ES);
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int kc = 0; kc < KC; ++kc)
-        buf[rb][kc] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff + 32 * kc * ES, 16 * rb * row_bytes,
-                                                             kStreamPolicy);
-  };
 
   f32x4 zacc[RB];
 #pragma unroll
@@ -608,15 +598,35 @@ ksweep_mfma_kernel(SweepArgs a) {
   const int n_full = a.d / kMTileC;
   const int t0 = strip * a.tps;
   const int t1 = min(t0 + a.tps, a.n_tiles);  // exclusive
-  uint16_t* tl = &lds_tile[wv][0];
   uint16_t* vl = &lds_v[wv][0];
 
+  __builtin_amdgcn_s_waitcnt(0);  // xs is read out before the first tile overwrites it
+  if (t0 < t1) stage_issue<DH, kStreamPolicy>(rsrc, tl, (uint32_t)(t0 * 128), row_bytes, lane);
 #pragma unroll 1
   for (int t = t0; t < t1; ++t) {
-    u32x4 cur[RB][KC];
-    load_tile(cur, t);
     const int c0 = t * kMTileC;
-    if (t >= n_full) {  // the ragged last tile: zero columns >= d
+    __builtin_amdgcn_s_waitcnt(0);  // tile t is in LDS
+    f32x4 d1[CB];
+    if (PROD1) {
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        d1[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+          d1[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              a1[kb], tr_read_staged(tl, 32 * kb + 8 * g + (s >> 2), 16 * cb + 4 * (s & 3)), d1[cb], 0, 0, 0);
+      }
+    }
+    u32x4 cur[RB][KC];
+    if (PROD2) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+        for (int kc = 0; kc < KC; ++kc) cur[rb][kc] = stage_chunk(tl, 16 * rb + s, 4 * kc + g);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // the tile is read out: stage the next one
+    if (t + 1 < t1) stage_issue<DH, kStreamPolicy>(rsrc, tl, (uint32_t)((t + 1) * 128), row_bytes, lane);
+    if (PROD2 && t >= n_full) {  // the ragged last tile: zero columns >= d
 #pragma unroll
       for (int kc = 0; kc < KC; ++kc) {
         const int nval = a.d - (c0 + 32 * kc + 8 * g);
@@ -631,34 +641,16 @@ ksweep_mfma_kernel(SweepArgs a) {
 
     bf16x8 b2[KC];
     if (PROD1) {
-      f32x4 d1[CB];
-#pragma unroll
-      for (int cb = 0; cb < CB; ++cb) d1[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int hf = 0; hf < NHALF; ++hf) {  // rows hf*SR .. hf*SR+SR-1 through LDS
-#pragma unroll
-        for (int rb = 0; rb < SR / 16; ++rb)
-#pragma unroll
-          for (int kc = 0; kc < KC; ++kc)
-            *reinterpret_cast<u32x4*>(tl + (16 * rb + s) * kMPitch + 32 * kc + 8 * g) = cur[hf * (SR / 16) + rb][kc];
-#pragma unroll
-        for (int cb = 0; cb < CB; ++cb)
-#pragma unroll
-          for (int kb = 0; kb < SR / 32; ++kb) {
-            const uint16_t* p = tl + (32 * kb + 8 * g + (s >> 2)) * kMPitch + 16 * cb + 4 * (s & 3);
-            d1[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[hf * (SR / 32) + kb], tr_read_8(p, p + 4 * kMPitch),
-                                                             d1[cb], 0, 0, 0);
-          }
-      }
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb) {
         // lane: column 16 cb + s; slots 4g .. 4g+3 = heads 2g (hi, lo), 2g+1 (hi, lo)
-        const float v0 = d1[cb][0] + d1[cb][1];
-        const float v1 = d1[cb][2] + d1[cb][3];
+        const int col = c0 + 16 * cb + s;
+        const bool inside = col < a.d;  // columns past d read the row's padding or the next row
+        const float v0 = inside ? d1[cb][0] + d1[cb][1] : 0.f;
+        const float v1 = inside ? d1[cb][2] + d1[cb][3] : 0.f;
         nrm0 = fmaf(v0, v0, nrm0);
         nrm1 = fmaf(v1, v1, nrm1);
-        const int col = c0 + 16 * cb + s;
-        if (col < a.d) {
+        if (inside) {
           if (last0) a.v[(size_t)(head0 + 2 * g) * a.d + col] = v0;
           if (last1) a.v[(size_t)(head0 + 2 * g + 1) * a.d + col] = v1;
         }

@@ -30,7 +30,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E, vendor figure
 METRIC = "heads·iters/sec (all layers) and achieved HBM GB/s vs MI355X peak"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "q_sweep_traffic.json")
-KERNEL_SRC = os.path.join(ROOT, "paper_2602_18851_amd", "csrc", "spectral.hip")
+KERNEL_DIR = os.path.join(ROOT, "paper_2602_18851_amd", "csrc")
 
 
 def parse():
@@ -72,8 +72,13 @@ def copy_reference(nbytes: int):
 
 
 def source_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of every kernel source and header: the counters are void once any changes."""
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(KERNEL_DIR)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            with open(os.path.join(KERNEL_DIR, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(kernel: str = ""):

@@ -1,0 +1,147 @@
+// Internal interface between the C ABI (spectral.hip) and the kernel sources
+// of the estimator (sweeps.hip, gram.hip, layer_form.hip): launch arguments,
+// workspace views, launch-shape constants and the launchers.  Not part of
+// the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace sn {
+
+constexpr int kWaves = 4;             // waves per workgroup
+constexpr int kThreads = 64 * kWaves;
+constexpr int kRG = 8;                // row groups per wave (lane >> 3)
+constexpr int kCPL = 8;               // 16-byte column chunks per wave row (lane & 7)
+constexpr int kMaxGC = 8;             // query heads per W_K work item
+constexpr int kQTargetItems = 16384;  // wave work items aimed for in a W_Q sweep
+constexpr int kKTargetItems = 4096;   // ... and in a W_K sweep (register-heavier waves)
+constexpr int kKMfmaResident = 2048;  // waves of the matrix-core W_K sweep resident at once (256 CUs x 8)
+constexpr int kStreamPolicy = 2;       // cache policy of the weight loads: non-temporal (read once per sweep)
+
+constexpr int kMWaves = 2;                 // waves per workgroup
+constexpr int kMTileC = 64;                // columns per tile: 128-byte row segments
+constexpr int kGWaves = 4;                 // waves per workgroup of the Gram sweep
+constexpr int kGTargetItems = 4096;        // Gram work items aimed for (about two waves per SIMD)
+constexpr int kRedThreads = 512;
+
+// Sweep phases: the first W_K sweep from v, the W_Q and W_K sweeps of a step,
+// and the two final sweeps of the Gram form (v' = K_j^T y and u' = Q_h^T z
+// from the d_h-vectors the Gram iteration leaves behind).
+enum { PH_INIT = 0, PH_Q = 1, PH_K = 2, PH_EK = 3, PH_EQ = 4 };
+enum { LM_ROWS = 0, LM_COLS = 1 };
+
+struct Work {
+  float* zp;         // [2][H][Sk][DH]  W_K-sweep partials of z, by step parity
+  float* zn;         // [2][H][Sk]      ... and of ||v'||^2 (||v||^2 for the first sweep)
+  float* yp;         // [H][Sq][DH]     W_Q-sweep partials of y
+  float* yn;         // [H][Sq]         ... and of ||u'||^2 = sigma^2
+  float* sig;        // [2][H]          sigma of the last two steps
+  float* vnorm0;     // [H]             ||v|| of the start vector
+  int32_t* alive;    // [2][H]          head continues after the step of that parity
+  int32_t* n_alive;  // [2]             heads still running after a W_K sweep
+  int32_t* iters;    // [H]             used when the caller passes no iters array
+  float* fin;        // [H][2][DH]      Gram form: z and y of each head's last step
+};
+
+struct SweepArgs {
+  const void* const* mats;  // device table: per-layer wq or wk
+  int64_t ld;
+  int32_t d, n_q, n_kv, g, H;
+  int32_t s_q, s_k;         // strips of the W_Q and W_K sweeps
+  int32_t s_out, tps, n_tiles, nch, n_items;
+  int32_t k, n_iter, want_vec;
+  float tol;
+  Work w;
+  float* v;
+  float* u;
+  float* sigma;
+  int32_t* iters;
+};
+
+struct FinArgs {
+  int32_t H, L, n_q, d, s_k;
+  int32_t slot_fixed;  // workspace slot of the ||v'||^2 partials; -1: parity of the last step
+  float coef;
+  Work w;
+  float* v;
+  float* u;
+  float* sigma;
+  float* scale;
+  int32_t* iters;
+};
+
+
+struct GramArgs {
+  const void* const* mats;  // device table: wq pointers of all layers, then wk pointers
+  int64_t ld;
+  int32_t d, L, n_q, n_kv, H;
+  int32_t s_g, tps, n_tiles, n_items;
+  float* gp;  // [units][s_g][NB][64 lanes][4]: partial Gram blocks in the MFMA output layout
+};
+
+struct IterArgs {
+  int32_t H, n_q, n_kv, g, s_k, s_g, n_iter;
+  float tol;
+  const float* gp;
+  Work w;
+  float* sigma;
+  int32_t* iters;
+};
+
+struct LayerArgs {
+  const void* const* mats;  // device table of this matrix's per-layer pointers
+  int64_t ld;
+  int32_t d, units, n_items, s_out, tps, n_tiles;
+  const int32_t* lstat;     // [L]
+  // rows sweep: x = xvec[layer] / sqrt(xn2[layer]) -> rowpart [L*units][s_out][DH]
+  const float* xvec;
+  const float* xn2;
+  float* rowpart;
+  // cols sweep: y = sum over y_cnt source units starting at (ul / y_div) * y_cnt
+  // of the source rows sweep's partials (y_units per layer, y_strips strips)
+  const float* ypart;
+  int32_t y_units, y_strips, y_div, y_cnt;
+  float* colout;            // [L*units][d]
+};
+
+// Per layer: vec[c] = sum over the layer's units of col[unit][c] (fixed order)
+// and n2 = ||vec||^2; mode 0 copies the caller's start vector instead and
+// (re)initialises the layer status; mode 1 marks M v = 0.
+struct LayerReduceArgs {
+  const float* col;
+  int32_t units, d, mode;
+  float* vec;
+  float* n2;
+  float* n2_start;  // mode 0: ||v||^2 of the start vector
+  int32_t* lstat;
+};
+
+// Outputs of the layer-level form: sigma, scale, v = v'/||v'||, u = u'/sigma.
+struct LayerFinArgs {
+  int32_t d, L;
+  float coef;
+  const int32_t* lstat;
+  const float* lu;
+  const float* lv;
+  const float* n2_u;
+  const float* n2_v;
+  const float* n2_start;
+  float* v;
+  float* u;
+  float* sigma;
+  float* scale;
+};
+
+// ---- launchers (one per kernel family; each picks the template instance)
+void launch_sweep(bool bf16, int head_dim, int ph, int gc, bool mfma, int n_items, hipStream_t st,
+                  const SweepArgs& a);
+void launch_finalize(int blocks, hipStream_t st, const FinArgs& f);
+void launch_gram(bool bf16, int head_dim, int n_items, hipStream_t st, const GramArgs& g);
+void launch_gram_iterate(int head_dim, int heads, hipStream_t st, const IterArgs& a);
+void launch_layer_sweep(bool bf16, int head_dim, int mode, int n_items, hipStream_t st, const LayerArgs& a);
+void launch_layer_reduce(int layers, hipStream_t st, const LayerReduceArgs& r);
+void launch_layer_finalize(int layers, hipStream_t st, const LayerFinArgs& f);
+
+}  // namespace sn

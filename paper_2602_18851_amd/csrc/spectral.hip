@@ -1,6 +1,8 @@
-// Per-head spectral norms of the query-key interaction matrices of every
-// attention layer by implicit power iteration, and the per-layer FP8 E4M3
-// scale factor, for MI355X (gfx950, wave64).
+// C ABI of the per-head spectral-norm estimator and the per-layer FP8 E4M3
+// scale factor for MI355X (gfx950): validation, workspace plan, context and
+// the entry points of include/spectral.h.  The kernels live in sweeps.hip
+// (the default form), gram.hip (SN_FLAG_GRAM), layer_form.hip
+// (spectral_step_layer) and logits_fp8.hip (spectral_logits_fp8).
 //
 // Method (arXiv 2602.18851, Sec. 4.1-4.2, App. E): for query head h with key
 // head j = floor(h / g), one step is
@@ -9,27 +11,6 @@
 // where Q_h, K_j are the d_h x d row blocks of the PyTorch-layout weights
 // (the transposes of the paper's W^Q_h, W^K_j) and M = Q_h^T K_j is never
 // formed.
-//
-// Schedule.  Each step is two fused sweeps over the weights:
-//   W_Q sweep (one wave per (head, column strip)): reads every Q_h element
-//     once, computes u'[c] = sum_r Q[r,c] z[r] for the strip's columns, its
-//     squared norm, and the d_h-vector partial y[r] = sum_c Q[r,c] u'[c].
-//   W_K sweep (one wave per (KV head, chunk of <= 8 query heads, strip)):
-//     reads every K_j element once and applies it to all query heads of the
-//     chunk from registers (the implicit-GQA form of Sec. 4.2 without key
-//     expansion): v'[c] = sum_r K[r,c] y_h[r], ||v'||^2, z_h[r] partials.
-// Partials (one d_h vector and one squared norm per strip) go to a small
-// workspace and are summed, in a fixed order, by the consumer of the next
-// sweep, which also normalises (y /= sigma, z /= ||v'||).  Every reduction
-// has a fixed order, so results are bitwise reproducible run to run.
-//
-// Wave tile.  A wave covers d_h rows x (8 chunks of 16 bytes) columns:
-// lane = 8 * rg + chunk, rows rg*RPL .. rg*RPL+RPL-1 (RPL = d_h / 8),
-// columns chunk*VEC .. +VEC-1 (VEC = 8 bf16 or 4 fp32).  Each load
-// instruction reads eight full 128-byte row segments.  The column sums of the
-// first product are reduced over the 8 row groups with lane shuffles
-// (xor 8, 16, 32), the row sums of the second product accumulate in registers
-// across the whole strip and are reduced over the 8 chunks once at its end.
 
 #include <hip/hip_runtime.h>
 
@@ -38,16 +19,15 @@
 #include <cstdint>
 #include <cstring>
 #include <string>
-#include <type_traits>
 #include <vector>
 
-#include "device_util.h"
+#include "kernels.h"
 #include "logits_fp8.h"
 #include "spectral.h"
 
 namespace {
 
-using namespace sn_dev;
+using namespace sn;
 
 thread_local std::string g_err;
 
@@ -63,1262 +43,11 @@ int fail(int code, const std::string& msg) {
       return fail(SN_EHIP, std::string(#expr) + " failed: " + hipGetErrorString(e_)); \
   } while (0)
 
-constexpr int kWaves = 4;             // waves per workgroup
-constexpr int kThreads = 64 * kWaves;
-constexpr int kRG = 8;                // row groups per wave (lane >> 3)
-constexpr int kCPL = 8;               // 16-byte column chunks per wave row (lane & 7)
-constexpr int kMaxGC = 8;             // query heads per W_K work item
-constexpr int kQTargetItems = 16384;  // wave work items aimed for in a W_Q sweep
-constexpr int kKTargetItems = 4096;   // ... and in a W_K sweep (register-heavier waves)
-constexpr int kKMfmaResident = 2048;  // waves of the matrix-core W_K sweep resident at once (256 CUs x 8)
-constexpr int kStreamPolicy = 2;       // cache policy of the weight loads: non-temporal (read once per sweep)
-
-// Sweep phases: the first W_K sweep from v, the W_Q and W_K sweeps of a step,
-// and the two final sweeps of the Gram form (v' = K_j^T y and u' = Q_h^T z
-// from the d_h-vectors the Gram iteration leaves behind).
-enum { PH_INIT = 0, PH_Q = 1, PH_K = 2, PH_EK = 3, PH_EQ = 4 };
 enum {
   KIND_INIT = 0, KIND_Q = 1, KIND_K = 2, KIND_FIN = 3, KIND_GRAM = 4, KIND_ITER = 5, KIND_EMIT = 6,
   KIND_LROWS = 7, KIND_LCOLS = 8, KIND_LRED = 9, KIND_PROJ = 10, KIND_LOGITS = 11, KIND_N = 12
 };
 static_assert(KIND_N == SN_PROFILE_KINDS, "profile kinds");
-
-struct Work {
-  float* zp;         // [2][H][Sk][DH]  W_K-sweep partials of z, by step parity
-  float* zn;         // [2][H][Sk]      ... and of ||v'||^2 (||v||^2 for the first sweep)
-  float* yp;         // [H][Sq][DH]     W_Q-sweep partials of y
-  float* yn;         // [H][Sq]         ... and of ||u'||^2 = sigma^2
-  float* sig;        // [2][H]          sigma of the last two steps
-  float* vnorm0;     // [H]             ||v|| of the start vector
-  int32_t* alive;    // [2][H]          head continues after the step of that parity
-  int32_t* n_alive;  // [2]             heads still running after a W_K sweep
-  int32_t* iters;    // [H]             used when the caller passes no iters array
-  float* fin;        // [H][2][DH]      Gram form: z and y of each head's last step
-};
-
-struct SweepArgs {
-  const void* const* mats;  // device table: per-layer wq or wk
-  int64_t ld;
-  int32_t d, n_q, n_kv, g, H;
-  int32_t s_q, s_k;         // strips of the W_Q and W_K sweeps
-  int32_t s_out, tps, n_tiles, nch, n_items;
-  int32_t k, n_iter, want_vec;
-  float tol;
-  Work w;
-  float* v;
-  float* u;
-  float* sigma;
-  int32_t* iters;
-};
-
-struct FinArgs {
-  int32_t H, L, n_q, d, s_k;
-  int32_t slot_fixed;  // workspace slot of the ||v'||^2 partials; -1: parity of the last step
-  float coef;
-  Work w;
-  float* v;
-  float* u;
-  float* sigma;
-  float* scale;
-  int32_t* iters;
-};
-
-template <typename T>
-struct Traits;
-template <>
-struct Traits<float> {
-  static constexpr int VEC = 4;
-};
-template <>
-struct Traits<uint16_t> {  // bf16 bit patterns
-  static constexpr int VEC = 8;
-};
-
-
-template <typename T>
-__device__ __forceinline__ float elem(const u32x4& q, int c);
-template <>
-__device__ __forceinline__ float elem<float>(const u32x4& q, int c) {
-  return __uint_as_float(q[c]);
-}
-template <>
-__device__ __forceinline__ float elem<uint16_t>(const u32x4& q, int c) {
-  const uint32_t w = q[c >> 1];
-  return __uint_as_float((c & 1) ? (w & 0xffff0000u) : (w << 16));
-}
-
-// Marks a chunk as redefined so the compiler re-derives its float values for
-// the second product instead of keeping all of them live across the lane
-// shuffles (that would double the register footprint of a tile).
-__device__ __forceinline__ void reuse_fence(u32x4& q) { asm volatile("" : "+v"(q)); }
-
-__device__ __forceinline__ float xor_sum(float x, int m) { return x + __shfl_xor(x, m); }
-
-// Sum over the 64 lanes of a wave (butterfly: every lane gets the same bits).
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) x += __shfl_xor(x, m);
-  return x;
-}
-
-// Occupancy floor per SIMD: the accumulators grow with GC * DH / 8 floats.
-template <int DH, int GC>
-constexpr int waves_hint() {
-  return GC * DH / kRG >= 128 ? 2 : GC * DH / kRG >= 64 ? 3 : 4;
-}
-
-// Sum over the 8 row groups of a wave tile (lanes that share lane mod 8):
-// the step inside a 16-lane row is a DPP row rotation by 8 fused into the
-// add; the steps across rows are lane shuffles.  Every lane ends with the
-// same total for its column.
-__device__ __forceinline__ float group_sum(float x) {
-  x += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x128, 0xF, 0xF, false));
-  x += __shfl_xor(x, 16);
-  x += __shfl_xor(x, 32);
-  return x;
-}
-
-// Work item of a sweep: which layer, which d_h-row block of that layer's
-// matrix, and which query heads (head0 .. head0 + nvalid - 1).
-struct Item {
-  int layer, row0, head0, nvalid, strip;
-};
-
-template <int DH, int GC, int PH>
-__device__ __forceinline__ Item decode_item(const SweepArgs& a, int item) {
-  Item it;
-  const bool valid_item = item < a.n_items;
-  it.strip = valid_item ? item % a.s_out : 0;
-  const int rest = valid_item ? item / a.s_out : 0;
-  if (PH == PH_Q || PH == PH_EQ) {  // one query head per item
-    it.layer = rest / a.n_q;
-    it.row0 = (rest % a.n_q) * DH;
-    it.head0 = rest;
-    it.nvalid = 1;
-  } else {
-    const int grp = rest / a.nch, ch = rest % a.nch;
-    it.layer = grp / a.n_kv;
-    const int j = grp % a.n_kv;
-    it.row0 = j * DH;
-    const int hin = ch * GC;
-    it.head0 = it.layer * a.n_q + j * a.g + hin;
-    it.nvalid = min(GC, a.g - hin);
-  }
-  if (!valid_item) it.nvalid = 0;
-  return it;
-}
-
-// Per-head bookkeeping at the start of a sweep (wave-uniform): which heads of
-// the item still iterate, which of them take their last step here (W_K
-// sweeps decide convergence, since sigma of the step is complete only after
-// the W_Q sweep), status / sigma / iteration outputs (written once, by the
-// strip-0 wave), and the normalised input vector of every active head, summed
-// over the producer's strips in a fixed order, into xs[i][0 .. d_h).
-template <int DH, int GC, int PH>
-__device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, int lane, float (*xs)[DH],
-                                           bool (&act)[GC], bool (&last)[GC]) {
-  const int strip = itm.strip, head0 = itm.head0, nvalid = itm.nvalid;
-  const int slot_prev = (a.k + 1) & 1;  // parity of step k-1
-  const int slot_cur = a.k & 1;
-  // ---- per-head decisions (wave-uniform) and normalised input vectors
-  int n_cont = 0;
-#pragma unroll
-  for (int i = 0; i < GC; ++i) {
-    act[i] = false;
-    last[i] = false;
-    if (i >= nvalid) continue;
-    const int hh = head0 + i;
-    if (PH == PH_INIT) {
-      act[i] = true;
-      if (strip == 0 && lane == 0) a.w.alive[hh] = 1;  // slot 0
-      continue;
-    }
-    if (PH == PH_EK || PH == PH_EQ) {  // final sweeps of the Gram form: heads that ran
-      act[i] = uni(a.iters[hh]) > 0;
-      last[i] = act[i];
-      if (act[i]) {
-        const float* src = a.w.fin + (size_t)hh * 2 * DH + (PH == PH_EK ? DH : 0);
-        for (int r = lane; r < DH; r += 64) xs[i][r] = src[r];
-      }
-      continue;
-    }
-    bool alive = uni(a.w.alive[slot_prev * a.H + hh]) != 0;
-    bool dead_v = false, dead_m = false;
-    float nv2 = 0.f;
-    if (a.k == 1) {
-      for (int s = 0; s < a.s_k; ++s) nv2 += a.w.zn[hh * a.s_k + s];
-      nv2 = uni(nv2);
-      if (!(nv2 > 0.f) || !isfinite(nv2)) {
-        alive = false;
-        dead_v = true;
-      }
-    }
-    float inv = 0.f;
-    const float* part = nullptr;
-    int s_in = 0;
-    if (PH == PH_Q) {
-      if (alive) {
-        float n2 = 0.f;
-        for (int s = 0; s < a.s_k; ++s) n2 += a.w.zn[(slot_prev * a.H + hh) * a.s_k + s];
-        inv = 1.0f / sqrtf(uni(n2));
-        part = a.w.zp + ((size_t)slot_prev * a.H + hh) * a.s_k * DH;
-        s_in = a.s_k;
-        act[i] = true;
-      }
-    } else {  // PH_K: sigma of this step is now complete
-      float sigma = 0.f;
-      if (alive) {
-        float s2 = 0.f;
-        for (int s = 0; s < a.s_q; ++s) s2 += a.w.yn[hh * a.s_q + s];
-        s2 = uni(s2);
-        sigma = sqrtf(s2);
-        if (s2 == 0.f) {
-          dead_m = true;
-        } else {
-          act[i] = true;
-          const float prev = uni(a.w.sig[slot_prev * a.H + hh]);
-          last[i] = (a.k >= a.n_iter) ||
-                    (a.tol > 0.f && a.k >= 2 && fabsf(sigma - prev) <= a.tol * sigma);
-          inv = 1.0f / sigma;
-          part = a.w.yp + (size_t)hh * a.s_q * DH;
-          s_in = a.s_q;
-        }
-      }
-      if (strip == 0 && lane == 0) {
-        if (a.k == 1) a.w.vnorm0[hh] = sqrtf(nv2);
-        if (dead_v) {
-          a.sigma[hh] = __builtin_nanf("");
-          a.iters[hh] = -1;
-        }
-        if (dead_m) {
-          a.sigma[hh] = 0.f;
-          a.iters[hh] = -2;
-        }
-        if (act[i]) {
-          a.w.sig[slot_cur * a.H + hh] = sigma;
-          if (last[i]) {
-            a.sigma[hh] = sigma;
-            a.iters[hh] = a.k;
-          }
-        }
-        a.w.alive[slot_cur * a.H + hh] = (act[i] && !last[i]) ? 1 : 0;
-      }
-      n_cont += (act[i] && !last[i]) ? 1 : 0;
-    }
-    if (PH == PH_Q && dead_v) act[i] = false;
-    if (act[i]) {
-      for (int r = lane; r < DH; r += 64) {
-        float s = 0.f;
-        for (int t = 0; t < s_in; ++t) s += part[t * DH + r];
-        xs[i][r] = s * inv;
-      }
-    }
-  }
-  if (PH == PH_K && strip == 0 && lane == 0 && n_cont > 0) atomicAdd(&a.w.n_alive[slot_cur], n_cont);
-}
-
-template <typename T, int DH, int GC, int PH>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_hint<DH, GC>())))
-sweep_kernel(SweepArgs a) {
-  constexpr int VEC = Traits<T>::VEC;
-  constexpr int CPL = kCPL;  // 16-byte column chunks per wave row: 128-byte row segments
-  constexpr int RPL = DH / kRG;
-  constexpr int TILE_C = CPL * VEC;
-  static_assert(DH % kRG == 0, "head_dim must be a multiple of 8");
-  __shared__ float xs[kWaves][GC][DH];
-
-  if (PH == PH_Q && blockIdx.x == 0 && threadIdx.x == 0) a.w.n_alive[a.k & 1] = 0;
-
-  const int lane = threadIdx.x & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
-  const int chunk = lane % CPL;
-  const int rg = lane / CPL;
-  const Item itm = decode_item<DH, GC, PH>(a, blockIdx.x * kWaves + wv);
-  const int layer = itm.layer, row0 = itm.row0, head0 = itm.head0, strip = itm.strip;
-  const int slot_cur = a.k & 1;
-  bool act[GC], last[GC];
-  head_setup<DH, GC, PH>(a, itm, lane, xs[wv], act, last);
-  __syncthreads();
-
-  bool any = false;
-#pragma unroll
-  for (int i = 0; i < GC; ++i) any |= act[i];
-  if (!any) return;
-
-  // Buffer resource over this head's (or KV head's) d_h x ld row block; the
-  // hardware range check returns zeros past the last valid element, and the
-  // per-row offsets ride in scalar registers.
-  constexpr int ES = sizeof(T);
-  const char* blk = uni(a.mats[layer]) + (int64_t)row0 * a.ld * ES;
-  // The range ends at the block's last valid element, rounded up to whole 16-byte
-  // chunks: the hardware drops a chunk that crosses the range end, and an aligned
-  // chunk that starts inside the matrix never leaves its memory page.
-  const uint32_t nrec = (uint32_t)((((int64_t)(DH - 1) * a.ld + a.d) * ES + 15) & ~int64_t(15));
-  const __amdgpu_buffer_rsrc_t rsrc =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(blk), (short)0, (int)nrec, kRsrcWord3);
-  const uint32_t lane_off = (uint32_t)(((int64_t)rg * RPL * a.ld + chunk * VEC) * ES);
-  const uint32_t row_bytes = (uint32_t)(a.ld * ES);
-
-  float xr1[GC == 1 ? RPL : 1];
-  if (GC == 1 && PH != PH_INIT) {
-#pragma unroll
-    for (int rr = 0; rr < (GC == 1 ? RPL : 1); ++rr) xr1[rr] = xs[wv][0][rg * RPL + rr];
-  }
-
-  float acc[GC][RPL];
-  float nrm[GC];
-#pragma unroll
-  for (int i = 0; i < GC; ++i) {
-    nrm[i] = 0.f;
-#pragma unroll
-    for (int rr = 0; rr < RPL; ++rr) acc[i][rr] = 0.f;
-  }
-
-  const int n_full = a.d / TILE_C;  // tiles whose columns are all inside d
-  const int t_first = strip * a.tps;
-  const int t_last = min(t_first + a.tps, a.n_tiles);  // exclusive
-  const int t_full_end = min(t_last, n_full);
-  const bool has_tail = t_last > n_full;               // the ragged last tile is ours
-
-  auto load_tile = [&](u32x4 (&tile)[RPL], int t) {
-    const uint32_t voff = lane_off + (uint32_t)(t * TILE_C * ES);
-#pragma unroll
-    for (int rr = 0; rr < RPL; ++rr)
-      tile[rr] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, rr * row_bytes, kStreamPolicy);
-  };
-  auto tile_step = [&](auto full_tag, int t, u32x4 (&tile)[RPL]) {
-    constexpr bool FULL = decltype(full_tag)::value;
-    const int col = t * TILE_C + chunk * VEC;
-    const int nval = FULL ? VEC : a.d - col;
-    if (!FULL) {
-      // the ragged tail: zero the elements at columns >= d (they belong to
-      // the row's padding, to the next row, or read as 0 past the range)
-      u32x4 m;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if (VEC == 8)
-          m[q] = (2 * q < nval ? 0x0000ffffu : 0u) | (2 * q + 1 < nval ? 0xffff0000u : 0u);
-        else
-          m[q] = q < nval ? 0xffffffffu : 0u;
-      }
-#pragma unroll
-      for (int rr = 0; rr < RPL; ++rr) tile[rr] &= m;
-    }
-
-#pragma unroll
-    for (int i = 0; i < GC; ++i) {
-      if (!act[i]) continue;
-      const int hh = head0 + i;
-      float w[VEC];
-      if (PH == PH_INIT) {
-        const float* vrow = a.v + (size_t)hh * a.d;
-#pragma unroll
-        for (int c = 0; c < VEC; ++c) {
-          const float x = vrow[FULL ? col + c : min(col + c, a.d - 1)];
-          w[c] = (FULL || c < nval) ? x : 0.f;
-        }
-      } else {
-#pragma unroll
-        for (int c = 0; c < VEC; ++c) w[c] = 0.f;
-#pragma unroll
-        for (int rr = 0; rr < RPL; ++rr) {
-          const float x = (GC == 1) ? xr1[GC == 1 ? rr : 0] : xs[wv][i][rg * RPL + rr];
-#pragma unroll
-          for (int c = 0; c < VEC; ++c) w[c] = fmaf(elem<T>(tile[rr], c), x, w[c]);
-        }
-#pragma unroll
-        for (int rr = 0; rr < RPL; ++rr) reuse_fence(tile[rr]);
-#pragma unroll
-        for (int c = 0; c < VEC; ++c) w[c] = group_sum(w[c]);
-      }
-#pragma unroll
-      for (int c = 0; c < VEC; ++c) nrm[i] = fmaf(w[c], w[c], nrm[i]);
-
-      // full d-space vector of the final step: v' (W_K sweep) or u' (W_Q sweep)
-      constexpr bool V_OUT = PH == PH_K || PH == PH_EK;
-      const bool write_vec = V_OUT ? last[i] : (PH == PH_EQ || (PH == PH_Q && a.want_vec));
-      if (write_vec && rg == 0) {
-        float* out = (V_OUT ? a.v : a.u) + (size_t)hh * a.d + col;
-#pragma unroll
-        for (int c = 0; c < VEC; ++c)
-          if (FULL || c < nval) out[c] = w[c];
-      }
-      // z of a finished head is not needed; the final sweeps produce no z or y
-      if ((PH == PH_K && last[i]) || PH == PH_EK || PH == PH_EQ) continue;
-#pragma unroll
-      for (int rr = 0; rr < RPL; ++rr) {
-        float s = acc[i][rr];
-#pragma unroll
-        for (int c = 0; c < VEC; ++c) s = fmaf(elem<T>(tile[rr], c), w[c], s);
-        acc[i][rr] = s;
-      }
-    }
-  };
-
-#pragma unroll 1
-  for (int t = t_first; t < t_full_end; ++t) {
-    u32x4 cur[RPL];
-    load_tile(cur, t);
-    tile_step(std::true_type{}, t, cur);
-  }
-  if (has_tail) {  // the ragged last tile
-    u32x4 cur[RPL];
-    load_tile(cur, n_full);
-    tile_step(std::false_type{}, n_full, cur);
-  }
-
-  if (PH == PH_EQ) return;  // u' is the only output
-  // ---- reduce over the 8 column chunks and write this strip's partials
-  float* outp = (PH == PH_Q) ? a.w.yp : a.w.zp + (size_t)slot_cur * a.H * a.s_k * DH;
-  float* outn = (PH == PH_Q) ? a.w.yn : a.w.zn + (size_t)slot_cur * a.H * a.s_k;
-#pragma unroll
-  for (int i = 0; i < GC; ++i) {
-    if (!act[i]) continue;
-    const int hh = head0 + i;
-    float n = nrm[i];  // row group 0's copy of the column sums
-#pragma unroll
-    for (int m = 1; m < CPL; m <<= 1) n = xor_sum(n, m);
-    if (lane == 0) outn[(size_t)hh * a.s_out + strip] = n;
-    if ((PH == PH_K && last[i]) || PH == PH_EK) continue;
-    float* op = outp + ((size_t)hh * a.s_out + strip) * DH + rg * RPL;
-#pragma unroll
-    for (int rr = 0; rr < RPL; ++rr) {
-      float s = acc[i][rr];
-#pragma unroll
-      for (int m = 1; m < CPL; m <<= 1) s = xor_sum(s, m);
-      if ((rr % CPL) == chunk) op[rr] = s;
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// W_K sweep on the matrix cores (bf16 weights, d_h in {64, 128}, groups of
-// 4..8 query heads).  With g heads sharing K_j, the sweep is a skinny dense
-// contraction: V' = K_j^T Y (d x g) and Z = K_j V' (d_h x g).  Both products
-// run as v_mfma_f32_16x16x32_bf16 with 16 "slots" = 8 heads x {hi, lo}: every
-// fp32 vector is split as x = hi + lo into two bf16 values (|x - hi - lo| <=
-// 2^-16 |x|) so the products keep ~16 significant bits while K stays in its
-// native bf16.
-//   Each tile (d_h rows x 64 columns of K_j) is staged once in LDS by
-//   coalesced loads (stage_issue) and read twice from there:
-//   Product 1 (contraction over rows) needs column fragments, read with
-//   ds_read_b64_tr_b16, which within each 16-lane group hands lane t element
-//   (t % 4) of source lane 4j + t / 4 for j = 0..3; pointing source lane s at
-//   row k0 + s / 4, column 4 (s % 4) gives lane t rows k0 .. k0 + 3 of
-//   column t.
-//   Product 2 (contraction over columns) reads the A-operand layout: lane
-//   16 g + s holds row s of a 16-row block and 8 consecutive columns.
-//   v' (16 slots x 64 columns) goes back through LDS to reach the B-operand
-//   layout of product 2.
-// The loads of tile t + 1 are in flight while tile t is multiplied.
-constexpr int kMWaves = 2;                 // waves per workgroup
-constexpr int kMTileC = 64;                // columns per tile: 128-byte row segments
-constexpr int kMVPitch = kMTileC + 8;      // LDS row pitch of the split v'
-
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-
-// Rows r and r + 4 of a staged tile, columns col .. col + 3, transposed over
-// each 16-lane group (see the comment above).
-__device__ __forceinline__ bf16x8 tr_read_staged(const uint8_t* tile, int r, int col) {
-  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-  const uint8_t* p0 = tile + 128 * r + 16 * ((col >> 3) ^ stage_swz(r)) + 2 * (col & 7);
-  const uint8_t* p1 = tile + 128 * (r + 4) + 16 * ((col >> 3) ^ stage_swz(r + 4)) + 2 * (col & 7);
-  const s16x4 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p0));
-  const s16x4 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p1));
-  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7));
-}
-
-template <int GC>
-__device__ __forceinline__ bool pick(const bool (&f)[GC], int i) {
-  bool r = false;
-#pragma unroll
-  for (int k = 0; k < GC; ++k) r |= (k == i) && f[k];
-  return r;
-}
-
-template <int DH, int PH>
-__global__ void __launch_bounds__(64 * kMWaves) __attribute__((amdgpu_waves_per_eu(2)))
-ksweep_mfma_kernel(SweepArgs a) {
-  constexpr int GC = 8;
-  constexpr int RB = DH / 16;          // 16-row blocks (product-2 M blocks)
-  constexpr int KB = DH / 32;          // 32-row blocks (product-1 K blocks)
-  constexpr int CB = kMTileC / 16;     // 16-column blocks (product-1 N blocks)
-  constexpr int KC = kMTileC / 32;     // 32-column blocks (product-2 K blocks)
-  constexpr int ES = 2;
-  static_assert(DH * 128 >= GC * DH * 4, "input vectors alias the tile buffer");
-  __shared__ __attribute__((aligned(16))) uint8_t lds_tile[kMWaves][DH * 128];
-  __shared__ __attribute__((aligned(16))) uint16_t lds_v[kMWaves][16 * kMVPitch];
-
-  const int lane = threadIdx.x & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int g = lane >> 4, s = lane & 15;
-  const Item itm = decode_item<DH, GC, PH>(a, blockIdx.x * kMWaves + wv);
-  const int head0 = itm.head0, strip = itm.strip;
-  const int slot_cur = a.k & 1;
-  uint8_t* tl = &lds_tile[wv][0];
-  float (*xs)[DH] = reinterpret_cast<float (*)[DH]>(tl);  // only until the first tile is staged
-  bool act[GC], last[GC];
-  head_setup<DH, GC, PH>(a, itm, lane, xs, act, last);
-  __syncthreads();
-  bool any = false;
-#pragma unroll
-  for (int i = 0; i < GC; ++i) any |= act[i];
-  if (!any) return;
-
-  // heads of this lane: product-1 outputs (columns) for heads 2g, 2g+1;
-  // B-operand / partial-sum slot s = head s/2, part s%2
-  const bool act0 = pick(act, 2 * g), act1 = pick(act, 2 * g + 1);
-  const bool last0 = pick(last, 2 * g), last1 = pick(last, 2 * g + 1);
-  const bool act_s = pick(act, s >> 1), last_s = pick(last, s >> 1);
-  const bool lo_part = (s & 1) != 0;
-
-  constexpr bool PROD1 = PH == PH_K || PH == PH_EK;  // v' = K^T y
-  constexpr bool PROD2 = PH != PH_EK;                // z = K v'
-  bf16x8 a1[KB];  // Y^T fragments: slot s, rows 32 kb + 8 g + t
-  if (PROD1) {
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const float y = act_s ? xs[s >> 1][32 * kb + 8 * g + t] : 0.f;
-        const __bf16 h = (__bf16)y;
-        a1[kb][t] = lo_part ? (__bf16)(y - (float)h) : h;
-      }
-  }
-
-  const char* blk = uni(a.mats[itm.layer]) + (int64_t)itm.row0 * a.ld * ES;
-  const uint32_t nrec = (uint32_t)((((int64_t)(DH - 1) * a.ld + a.d) * ES + 15) & ~int64_t(15));
-  const __amdgpu_buffer_rsrc_t rsrc = make_rsrc(blk, nrec);
-  const uint32_t row_bytes = (uint32_t)(a.ld * ES);
-
-  f32x4 zacc[RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) zacc[rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float nrm0 = 0.f, nrm1 = 0.f;
-  const int n_full = a.d / kMTileC;
-  const int t0 = strip * a.tps;
-  const int t1 = min(t0 + a.tps, a.n_tiles);  // exclusive
-  uint16_t* vl = &lds_v[wv][0];
-
-  __builtin_amdgcn_s_waitcnt(0);  // xs is read out before the first tile overwrites it
-  if (t0 < t1) stage_issue<DH, kStreamPolicy>(rsrc, tl, (uint32_t)(t0 * 128), row_bytes, lane);
-#pragma unroll 1
-  for (int t = t0; t < t1; ++t) {
-    const int c0 = t * kMTileC;
-    __builtin_amdgcn_s_waitcnt(0);  // tile t is in LDS
-    f32x4 d1[CB];
-    if (PROD1) {
-#pragma unroll
-      for (int cb = 0; cb < CB; ++cb) {
-        d1[cb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
-          d1[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              a1[kb], tr_read_staged(tl, 32 * kb + 8 * g + (s >> 2), 16 * cb + 4 * (s & 3)), d1[cb], 0, 0, 0);
-      }
-    }
-    u32x4 cur[RB][KC];
-    if (PROD2) {
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int kc = 0; kc < KC; ++kc) cur[rb][kc] = stage_chunk(tl, 16 * rb + s, 4 * kc + g);
-    }
-    __builtin_amdgcn_s_waitcnt(0);  // the tile is read out: stage the next one
-    if (t + 1 < t1) stage_issue<DH, kStreamPolicy>(rsrc, tl, (uint32_t)((t + 1) * 128), row_bytes, lane);
-    if (PROD2 && t >= n_full) {  // the ragged last tile: zero columns >= d
-#pragma unroll
-      for (int kc = 0; kc < KC; ++kc) {
-        const int nval = a.d - (c0 + 32 * kc + 8 * g);
-        u32x4 m;
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          m[q] = (2 * q < nval ? 0x0000ffffu : 0u) | (2 * q + 1 < nval ? 0xffff0000u : 0u);
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) cur[rb][kc] &= m;
-      }
-    }
-
-    bf16x8 b2[KC];
-    if (PROD1) {
-#pragma unroll
-      for (int cb = 0; cb < CB; ++cb) {
-        // lane: column 16 cb + s; slots 4g .. 4g+3 = heads 2g (hi, lo), 2g+1 (hi, lo)
-        const int col = c0 + 16 * cb + s;
-        const bool inside = col < a.d;  // columns past d read the row's padding or the next row
-        const float v0 = inside ? d1[cb][0] + d1[cb][1] : 0.f;
-        const float v1 = inside ? d1[cb][2] + d1[cb][3] : 0.f;
-        nrm0 = fmaf(v0, v0, nrm0);
-        nrm1 = fmaf(v1, v1, nrm1);
-        if (inside) {
-          if (last0) a.v[(size_t)(head0 + 2 * g) * a.d + col] = v0;
-          if (last1) a.v[(size_t)(head0 + 2 * g + 1) * a.d + col] = v1;
-        }
-        if (!PROD2) continue;
-        const __bf16 h0 = (__bf16)v0, h1 = (__bf16)v1;
-        const __bf16 l0 = (__bf16)(v0 - (float)h0), l1 = (__bf16)(v1 - (float)h1);
-        const int c = 16 * cb + s;
-        vl[(4 * g + 0) * kMVPitch + c] = __builtin_bit_cast(uint16_t, h0);
-        vl[(4 * g + 1) * kMVPitch + c] = __builtin_bit_cast(uint16_t, l0);
-        vl[(4 * g + 2) * kMVPitch + c] = __builtin_bit_cast(uint16_t, h1);
-        vl[(4 * g + 3) * kMVPitch + c] = __builtin_bit_cast(uint16_t, l1);
-      }
-      if (PROD2) {
-#pragma unroll
-        for (int kc = 0; kc < KC; ++kc)
-          b2[kc] = *reinterpret_cast<const bf16x8*>(vl + s * kMVPitch + 32 * kc + 8 * g);
-      }
-    } else {  // first sweep: v' is the start vector itself
-      const float* vrow = a.v + (size_t)(head0 + (s >> 1)) * a.d;
-#pragma unroll
-      for (int kc = 0; kc < KC; ++kc)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int col = c0 + 32 * kc + 8 * g + e;
-          const float x = (act_s && col < a.d) ? vrow[min(col, a.d - 1)] : 0.f;
-          if (!lo_part) nrm0 = fmaf(x, x, nrm0);
-          const __bf16 h = (__bf16)x;
-          b2[kc][e] = lo_part ? (__bf16)(x - (float)h) : h;
-        }
-    }
-
-    if (PROD2) {
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int kc = 0; kc < KC; ++kc)
-          zacc[rb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, cur[rb][kc]), b2[kc],
-                                                             zacc[rb], 0, 0, 0);
-    }
-  }
-
-  // ---- partials of this strip
-  float* zp_out = a.w.zp + (size_t)slot_cur * a.H * a.s_k * DH;
-  float* zn_out = a.w.zn + (size_t)slot_cur * a.H * a.s_k;
-  // z = hi-slot + lo-slot (lanes s, s ^ 1); even lanes own head s / 2
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) zacc[rb][j] += __shfl_xor(zacc[rb][j], 1);
-  if (PROD2 && !lo_part && act_s && !last_s) {
-    float* op = zp_out + ((size_t)(head0 + (s >> 1)) * a.s_out + strip) * DH + 4 * g;
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) *reinterpret_cast<f32x4*>(op + 16 * rb) = zacc[rb];
-  }
-  if (PROD1) {  // lane (g, s) summed columns of heads 2g, 2g+1: reduce over s
-#pragma unroll
-    for (int m = 1; m < 16; m <<= 1) {
-      nrm0 += __shfl_xor(nrm0, m);
-      nrm1 += __shfl_xor(nrm1, m);
-    }
-    if (s == 0) {
-      if (act0) zn_out[(size_t)(head0 + 2 * g) * a.s_out + strip] = nrm0;
-      if (act1) zn_out[(size_t)(head0 + 2 * g + 1) * a.s_out + strip] = nrm1;
-    }
-  } else {  // part-0 lanes of head s/2 summed disjoint columns: reduce over g
-    nrm0 += __shfl_xor(nrm0, 16);
-    nrm0 += __shfl_xor(nrm0, 32);
-    if (g == 0 && !lo_part && act_s) zn_out[(size_t)(head0 + (s >> 1)) * a.s_out + strip] = nrm0;
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Gram form (SN_FLAG_GRAM).  With G_Q = Q_h Q_h^T and G_K = K_j K_j^T
-// (d_h x d_h), one step of the iteration is
-//     w = G_Q z,  sigma^2 = z^T w,  y = w / sigma,
-//     t = G_K y,  ||v'||^2 = y^T t,  z_next = t / ||v'||,
-// because u' = Q_h^T z has ||u'||^2 = z^T G_Q z and Q_h u' = G_Q z, and
-// likewise for v' = K_j^T y.  These are the iterates of the sweeps above,
-// computed in d_h-space.
-//
-// gram_kernel forms G = R R^T for every d_h x d row block R (query heads
-// first, then key heads) on the matrix cores: an output block (bi, bj) of
-// 16 x 16 is one MFMA chain whose A operand is rows 16 bi.. of R and whose B
-// operand is rows 16 bj.. of R, both in the rows' native layout (lane l
-// holds row l % 16 and 16 bytes of consecutive columns; the contraction
-// index may be permuted freely as long as both operands share it).  Only the
-// upper triangle of blocks is formed.  A wave streams its rows through LDS in
-// tiles of 128-byte row segments (coalesced loads; see stage_issue) and reads
-// the operands back in the MFMA layout.
-constexpr int kGWaves = 4;                 // waves per workgroup of the Gram sweep
-constexpr int kGTargetItems = 4096;        // Gram work items aimed for (about two waves per SIMD)
-
-struct GramArgs {
-  const void* const* mats;  // device table: wq pointers of all layers, then wk pointers
-  int64_t ld;
-  int32_t d, L, n_q, n_kv, H;
-  int32_t s_g, tps, n_tiles, n_items;
-  float* gp;  // [units][s_g][NB][64 lanes][4]: partial Gram blocks in the MFMA output layout
-};
-
-template <int RB>
-__host__ __device__ constexpr int tri_index(int bi, int bj) {  // bj >= bi
-  return bi * RB - bi * (bi - 1) / 2 + (bj - bi);
-}
-
-template <typename T, int DH>
-__global__ void __launch_bounds__(64 * kGWaves) __attribute__((amdgpu_waves_per_eu(DH >= 128 ? 2 : 4)))
-gram_kernel(GramArgs a) {
-  constexpr int ES = sizeof(T);
-  constexpr int RB = DH / 16;
-  constexpr int NB = RB * (RB + 1) / 2;
-  constexpr int TC = 128 / ES;  // columns per tile
-  __shared__ __attribute__((aligned(16))) uint8_t stage[kGWaves][DH * 128];
-  const int lane = threadIdx.x & 63;
-  const int wv = uni((int)(threadIdx.x >> 6));
-  const int q = lane >> 4, s = lane & 15;
-  const int item = blockIdx.x * kGWaves + wv;
-  if (item >= a.n_items) return;
-  const int unit = item / a.s_g, strip = item % a.s_g;
-  int layer, row0, tab;
-  if (unit < a.H) {
-    layer = unit / a.n_q;
-    row0 = (unit % a.n_q) * DH;
-    tab = layer;
-  } else {
-    layer = (unit - a.H) / a.n_kv;
-    row0 = ((unit - a.H) % a.n_kv) * DH;
-    tab = a.L + layer;
-  }
-  const char* blk = uni(a.mats[tab]) + (int64_t)row0 * a.ld * ES;
-  const uint32_t nrec = (uint32_t)((((int64_t)(DH - 1) * a.ld + a.d) * ES + 15) & ~int64_t(15));
-  const __amdgpu_buffer_rsrc_t rsrc =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(blk), (short)0, (int)nrec, kRsrcWord3);
-  const uint32_t row_bytes = (uint32_t)(a.ld * ES);
-  uint8_t* tile = stage[wv];
-
-  f32x4 acc[NB];
-#pragma unroll
-  for (int b = 0; b < NB; ++b) acc[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int n_full = a.d / TC;
-  const int t0 = strip * a.tps;
-  const int t1 = min(t0 + a.tps, a.n_tiles);
-
-  // one LDS tile per wave: tile t + 1 streams in while tile t is multiplied
-  // from registers
-  if (t0 < t1) stage_issue<DH, kStreamPolicy>(rsrc, tile, (uint32_t)(t0 * 128), row_bytes, lane);
-#pragma unroll 1
-  for (int t = t0; t < t1; ++t) {
-    __builtin_amdgcn_s_waitcnt(0);  // the tile is in LDS
-    u32x4 fr[RB][2];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int kc = 0; kc < 2; ++kc) fr[rb][kc] = stage_chunk(tile, 16 * rb + s, 4 * kc + q);
-    __builtin_amdgcn_s_waitcnt(0);  // read out before the next tile overwrites it
-    if (t + 1 < t1) stage_issue<DH, kStreamPolicy>(rsrc, tile, (uint32_t)((t + 1) * 128), row_bytes, lane);
-    if (t >= n_full) {  // the ragged last tile: zero columns >= d
-#pragma unroll
-      for (int kc = 0; kc < 2; ++kc) {
-        const int nval = a.d - (t * TC + (64 * kc + 16 * q) / ES);
-        u32x4 m;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          if (ES == 2)
-            m[e] = (2 * e < nval ? 0x0000ffffu : 0u) | (2 * e + 1 < nval ? 0xffff0000u : 0u);
-          else
-            m[e] = e < nval ? 0xffffffffu : 0u;
-        }
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) fr[rb][kc] &= m;
-      }
-    }
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-      for (int bi = 0; bi < RB; ++bi)
-#pragma unroll
-        for (int bj = bi; bj < RB; ++bj) {
-          f32x4& c = acc[tri_index<RB>(bi, bj)];
-          if constexpr (ES == 2) {
-            c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, fr[bi][kc]),
-                                                        __builtin_bit_cast(bf16x8, fr[bj][kc]), c, 0, 0, 0);
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(fr[bi][kc][e]),
-                                                       __uint_as_float(fr[bj][kc][e]), c, 0, 0, 0);
-          }
-        }
-  }
-  f32x4* out = reinterpret_cast<f32x4*>(a.gp) + ((size_t)item * NB) * 64 + lane;
-#pragma unroll
-  for (int b = 0; b < NB; ++b) out[(size_t)b * 64] = acc[b];
-}
-
-// d_h-space iteration of the Gram form: one workgroup of NT threads per query
-// head.  Thread t = 16 R + C owns rows RPT R .. RPT R + RPT - 1 and columns
-// CPT C .. CPT C + CPT - 1 (CPT = d_h / 16) of G_Q and of G_K in registers.
-// A product G x reads CPT entries of x from LDS and sums the partial rows
-// over the 16 lanes C = 0..15 of a DPP row with a butterfly (quad xor 1,
-// xor 2, half-row mirror, row mirror) that leaves the same bits in every
-// lane.  Norms are summed in a fixed order, and every thread takes the same
-// per-head decisions from the same values.
-struct IterArgs {
-  int32_t H, n_q, n_kv, g, s_k, s_g, n_iter;
-  float tol;
-  const float* gp;
-  Work w;
-  float* sigma;
-  int32_t* iters;
-};
-
-template <int DH>
-struct IterShape {
-  static constexpr int RPT = DH >= 32 ? DH / 32 : 1;  // rows per thread
-  static constexpr int CPT = DH / 16;                 // columns per thread
-  static constexpr int NT = 16 * DH / RPT;            // threads per workgroup
-  static constexpr int NW = NT / 64;                  // waves per workgroup
-  static constexpr int RB = DH / 16, NB = RB * (RB + 1) / 2;
-};
-
-template <int CTRL>
-__device__ __forceinline__ float dpp_add(float x) {
-  return x + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
-}
-
-// Sum over the 16 lanes of a DPP row; every lane of the row gets the same bits.
-__device__ __forceinline__ float row16_sum(float x) {
-  x = dpp_add<0xB1>(x);   // quad_perm [1, 0, 3, 2]
-  x = dpp_add<0x4E>(x);   // quad_perm [2, 3, 0, 1]
-  x = dpp_add<0x141>(x);  // row_half_mirror: quad 0 <-> 1, 2 <-> 3
-  x = dpp_add<0x140>(x);  // row_mirror: half 0 <-> half 1
-  return x;
-}
-
-// Sum of the values of lanes 0, 16, 32, 48 (the C == 0 lanes), in that order.
-__device__ __forceinline__ float c0_lanes_sum(float x) {
-  const int b = __builtin_bit_cast(int, x);
-  return (__builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 0)) +
-          __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 16))) +
-         (__builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 32)) +
-          __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 48)));
-}
-
-template <int NW>
-__device__ __forceinline__ float sum_waves(const float* red) {
-  float s = 0.f;
-#pragma unroll
-  for (int w = 0; w < NW; ++w) s += red[w];
-  return s;
-}
-
-// Sums the strips of one Gram matrix (upper-triangle 16 x 16 blocks in the
-// MFMA output layout), writes the whole symmetric matrix to LDS and hands
-// each thread its RPT x CPT sub-block.
-template <int DH>
-__device__ __forceinline__ void gram_to_regs(const float* src, int s_g, float* gl,
-                                             float (&reg)[IterShape<DH>::RPT][IterShape<DH>::CPT]) {
-  using S = IterShape<DH>;
-  constexpr int P = DH + 1, NE = S::NB * 256, NL = (NE + S::NT - 1) / S::NT;
-  const int t = threadIdx.x;
-  float x[NL];  // flat elements t, t + NT, ... of the blocks, summed over the strips
-#pragma unroll
-  for (int m = 0; m < NL; ++m) x[m] = (m * S::NT + t < NE) ? src[m * S::NT + t] : 0.f;
-  for (int st = 1; st < s_g; ++st) {
-#pragma unroll
-    for (int m = 0; m < NL; ++m)
-      if (m * S::NT + t < NE) x[m] += src[(size_t)st * NE + m * S::NT + t];
-  }
-#pragma unroll
-  for (int m = 0; m < NL; ++m) {
-    const int f = m * S::NT + t;
-    if (f >= NE) continue;
-    const int b = f >> 8, ln = (f & 255) >> 2, e = f & 3;  // block, lane and element in the MFMA layout
-    int bi = 0, start = 0;
-    while (b >= start + (S::RB - bi)) {  // upper-triangle block b -> (bi, bj)
-      start += S::RB - bi;
-      ++bi;
-    }
-    const int bj = bi + (b - start);
-    const int r = 16 * bi + 4 * (ln >> 4) + e, c = 16 * bj + (ln & 15);
-    gl[r * P + c] = x[m];
-    if (bi != bj) gl[c * P + r] = x[m];
-  }
-  __syncthreads();
-  const int R = t >> 4, C = t & 15;
-#pragma unroll
-  for (int i = 0; i < S::RPT; ++i)
-#pragma unroll
-    for (int j = 0; j < S::CPT; ++j) reg[i][j] = gl[(S::RPT * R + i) * P + S::CPT * C + j];
-  __syncthreads();
-}
-
-// out[i] = sum_c G[RPT R + i][c] x[c], complete in every lane of the row.
-template <int RPT, int CPT>
-__device__ __forceinline__ void gram_matvec(const float (&g)[RPT][CPT], const float* x, int C, float (&out)[RPT]) {
-  float xv[CPT];
-#pragma unroll
-  for (int j = 0; j < CPT; ++j) xv[j] = x[CPT * C + j];
-#pragma unroll
-  for (int i = 0; i < RPT; ++i) {
-    float acc = 0.f;
-#pragma unroll
-    for (int j = 0; j < CPT; ++j) acc = fmaf(g[i][j], xv[j], acc);
-    out[i] = row16_sum(acc);
-  }
-}
-
-template <int DH>
-__global__ void __launch_bounds__(IterShape<DH>::NT) gram_iterate_kernel(IterArgs a) {
-  using S = IterShape<DH>;
-  constexpr int RPT = S::RPT, CPT = S::CPT, NW = S::NW;
-  __shared__ float gl[DH * (DH + 1)];
-  __shared__ float wb[DH], tb[DH];
-  __shared__ float red_a[NW], red_b[NW];
-  const int h = blockIdx.x, t = threadIdx.x, lane = t & 63, wv = t >> 6;
-  const int R = t >> 4, C = t & 15;
-  const int layer = h / a.n_q;
-  const int j = layer * a.n_kv + (h % a.n_q) / a.g;
-
-  // start vector: ||v||^2 and z = K_j v from the first W_K sweep (slot 0)
-  float nv2 = 0.f;
-  for (int st = 0; st < a.s_k; ++st) nv2 += a.w.zn[(size_t)h * a.s_k + st];
-  if (t == 0) a.w.vnorm0[h] = sqrtf(nv2);
-  if (!(nv2 > 0.f) || !isfinite(nv2)) {
-    if (t == 0) {
-      a.sigma[h] = __builtin_nanf("");
-      a.iters[h] = -1;
-    }
-    return;
-  }
-  const float inv0 = 1.0f / sqrtf(nv2);
-  if (t < DH) {
-    float z = 0.f;
-    for (int st = 0; st < a.s_k; ++st) z += a.w.zp[((size_t)h * a.s_k + st) * DH + t];
-    tb[t] = z * inv0;
-  }
-  float gq[RPT][CPT], gk[RPT][CPT];
-  gram_to_regs<DH>(a.gp + (size_t)h * a.s_g * S::NB * 256, a.s_g, gl, gq);
-  gram_to_regs<DH>(a.gp + (size_t)(a.H + j) * a.s_g * S::NB * 256, a.s_g, gl, gk);
-
-  float zscale = 1.f, prev = 0.f;
-  float out[RPT];
-#pragma unroll 1
-  for (int k = 1;; ++k) {
-    // w = G_Q z with z = zscale * tb; lane C == 0 of row band R owns rows RPT R ..
-    gram_matvec<RPT, CPT>(gq, tb, C, out);
-    float part = 0.f;
-    if (C == 0) {
-#pragma unroll
-      for (int i = 0; i < RPT; ++i) {
-        const float wr = out[i] * zscale;
-        part = fmaf(tb[RPT * R + i] * zscale, wr, part);
-        wb[RPT * R + i] = wr;
-      }
-    }
-    part = c0_lanes_sum(part);
-    if (lane == 0) red_a[wv] = part;
-    __syncthreads();
-    const float s2 = sum_waves<NW>(red_a);
-    const float sig = sqrtf(s2);
-    if (s2 == 0.f) {  // M v = 0
-      if (t == 0) {
-        a.sigma[h] = 0.f;
-        a.iters[h] = -2;
-      }
-      return;
-    }
-    const bool last = (k >= a.n_iter) || (a.tol > 0.f && k >= 2 && fabsf(sig - prev) <= a.tol * sig);
-    const float inv = 1.0f / sig;
-    if (last) {
-      if (t < DH) {
-        a.w.fin[(size_t)h * 2 * DH + t] = tb[t] * zscale;     // z of the last step
-        a.w.fin[(size_t)h * 2 * DH + DH + t] = wb[t] * inv;   // y = Q_h u
-      }
-      if (t == 0) {
-        a.sigma[h] = sig;
-        a.iters[h] = k;
-      }
-      return;
-    }
-    // t = G_K y with y = w / sigma
-    gram_matvec<RPT, CPT>(gk, wb, C, out);
-    float part2 = 0.f;
-    if (C == 0) {
-#pragma unroll
-      for (int i = 0; i < RPT; ++i) {
-        const float tr = out[i] * inv;
-        part2 = fmaf(wb[RPT * R + i] * inv, tr, part2);
-        tb[RPT * R + i] = tr;
-      }
-    }
-    part2 = c0_lanes_sum(part2);
-    if (lane == 0) red_b[wv] = part2;
-    __syncthreads();
-    const float n2 = sum_waves<NW>(red_b);
-    zscale = 1.0f / sqrtf(n2);
-    prev = sig;
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Layer-level form (spectral_step_layer): the estimator as printed in App. E,
-// one pair u, v in R^d per layer for the concatenated W^Q = [W^Q_1 .. W^Q_nq]
-// and the key blocks repeated per group (RepeatBlocks) on the way in and
-// summed per group (SumGroups) on the way back.  One step is four sweeps:
-//   rows(W_K, v):  z_j = K_j v                     (row sums, per key head)
-//   cols(W_Q, z):  c_h = Q_h^T z_{j(h)}            (column sums, per query head)
-//   u' = sum_h c_h, sigma = ||u'||                 (layer_reduce_kernel)
-//   rows(W_Q, u):  y_h = Q_h u'/sigma
-//   cols(W_K, y):  c_j = K_j^T sum_{h in group j} y_h
-//   v' = sum_j c_j                                 (layer_reduce_kernel)
-// A column sweep item owns whole columns of its unit, so it writes its part
-// of c without partials; the per-layer sum over units runs in a fixed order.
-// Per-layer status: 0 running, -1 start vector zero or not finite, -2 M v = 0.
-enum { LM_ROWS = 0, LM_COLS = 1 };
-
-struct LayerArgs {
-  const void* const* mats;  // device table of this matrix's per-layer pointers
-  int64_t ld;
-  int32_t d, units, n_items, s_out, tps, n_tiles;
-  const int32_t* lstat;     // [L]
-  // rows sweep: x = xvec[layer] / sqrt(xn2[layer]) -> rowpart [L*units][s_out][DH]
-  const float* xvec;
-  const float* xn2;
-  float* rowpart;
-  // cols sweep: y = sum over y_cnt source units starting at (ul / y_div) * y_cnt
-  // of the source rows sweep's partials (y_units per layer, y_strips strips)
-  const float* ypart;
-  int32_t y_units, y_strips, y_div, y_cnt;
-  float* colout;            // [L*units][d]
-};
-
-template <typename T, int DH, int MODE>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4)))
-layer_sweep_kernel(LayerArgs a) {
-  constexpr int VEC = Traits<T>::VEC;
-  constexpr int CPL = kCPL;
-  constexpr int RPL = DH / kRG;
-  constexpr int TILE_C = CPL * VEC;
-  constexpr int ES = sizeof(T);
-  __shared__ float xs[kWaves][DH];
-  const int lane = threadIdx.x & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int chunk = lane % CPL, rg = lane / CPL;
-  const int item = blockIdx.x * kWaves + wv;
-  const bool in_range = item < a.n_items;
-  const int unit = in_range ? item / a.s_out : 0;
-  const int strip = in_range ? item % a.s_out : 0;
-  const int layer = unit / a.units, ul = unit % a.units;
-  const bool valid = in_range && uni(a.lstat[layer]) == 0;
-  if (MODE == LM_COLS && valid) {
-    const int src0 = layer * a.y_units + (ul / a.y_div) * a.y_cnt;
-    for (int r = lane; r < DH; r += 64) {
-      float s = 0.f;
-      for (int i = 0; i < a.y_cnt; ++i)
-        for (int st = 0; st < a.y_strips; ++st) s += a.ypart[((size_t)(src0 + i) * a.y_strips + st) * DH + r];
-      xs[wv][r] = s;
-    }
-  }
-  __syncthreads();
-  if (!valid) return;
-
-  const char* blk = uni(a.mats[layer]) + (int64_t)ul * DH * a.ld * ES;
-  const uint32_t nrec = (uint32_t)((((int64_t)(DH - 1) * a.ld + a.d) * ES + 15) & ~int64_t(15));
-  const __amdgpu_buffer_rsrc_t rsrc =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(blk), (short)0, (int)nrec, kRsrcWord3);
-  const uint32_t lane_off = (uint32_t)(((int64_t)rg * RPL * a.ld + chunk * VEC) * ES);
-  const uint32_t row_bytes = (uint32_t)(a.ld * ES);
-
-  float yr[MODE == LM_COLS ? RPL : 1];
-  if (MODE == LM_COLS) {
-#pragma unroll
-    for (int rr = 0; rr < (MODE == LM_COLS ? RPL : 1); ++rr) yr[rr] = xs[wv][rg * RPL + rr];
-  }
-  const float* xrow = a.xvec + (size_t)layer * a.d;
-  float acc[RPL];
-#pragma unroll
-  for (int rr = 0; rr < RPL; ++rr) acc[rr] = 0.f;
-
-  const int n_full = a.d / TILE_C;
-  const int t0 = strip * a.tps;
-  const int t1 = min(t0 + a.tps, a.n_tiles);
-#pragma unroll 1
-  for (int t = t0; t < t1; ++t) {
-    u32x4 tile[RPL];
-    const uint32_t voff = lane_off + (uint32_t)(t * TILE_C * ES);
-#pragma unroll
-    for (int rr = 0; rr < RPL; ++rr)
-      tile[rr] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, rr * row_bytes, kStreamPolicy);
-    const int col = t * TILE_C + chunk * VEC;
-    const int nval = a.d - col;  // >= VEC on full tiles
-    if (t >= n_full) {
-      u32x4 m;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if (VEC == 8)
-          m[q] = (2 * q < nval ? 0x0000ffffu : 0u) | (2 * q + 1 < nval ? 0xffff0000u : 0u);
-        else
-          m[q] = q < nval ? 0xffffffffu : 0u;
-      }
-#pragma unroll
-      for (int rr = 0; rr < RPL; ++rr) tile[rr] &= m;
-    }
-    if (MODE == LM_ROWS) {
-      float xv[VEC];
-#pragma unroll
-      for (int c = 0; c < VEC; ++c) xv[c] = c < nval ? xrow[min(col + c, a.d - 1)] : 0.f;
-#pragma unroll
-      for (int rr = 0; rr < RPL; ++rr) {
-        float s = acc[rr];
-#pragma unroll
-        for (int c = 0; c < VEC; ++c) s = fmaf(elem<T>(tile[rr], c), xv[c], s);
-        acc[rr] = s;
-      }
-    } else {
-      float w[VEC];
-#pragma unroll
-      for (int c = 0; c < VEC; ++c) w[c] = 0.f;
-#pragma unroll
-      for (int rr = 0; rr < RPL; ++rr)
-#pragma unroll
-        for (int c = 0; c < VEC; ++c) w[c] = fmaf(elem<T>(tile[rr], c), yr[MODE == LM_COLS ? rr : 0], w[c]);
-#pragma unroll
-      for (int c = 0; c < VEC; ++c) w[c] = group_sum(w[c]);
-      if (rg == 0) {
-        float* out = a.colout + (size_t)unit * a.d + col;
-#pragma unroll
-        for (int c = 0; c < VEC; ++c)
-          if (c < nval) out[c] = w[c];
-      }
-    }
-  }
-  if (MODE == LM_ROWS) {
-    const float xs_inv = 1.0f / sqrtf(a.xn2[layer]);
-    float* op = a.rowpart + ((size_t)unit * a.s_out + strip) * DH + rg * RPL;
-#pragma unroll
-    for (int rr = 0; rr < RPL; ++rr) {
-      float s = acc[rr];
-#pragma unroll
-      for (int m = 1; m < CPL; m <<= 1) s = xor_sum(s, m);
-      if ((rr % CPL) == chunk) op[rr] = s * xs_inv;
-    }
-  }
-}
-
-// Per layer: vec[c] = sum over the layer's units of col[unit][c] (fixed order)
-// and n2 = ||vec||^2; mode 0 copies the caller's start vector instead and
-// (re)initialises the layer status; mode 1 marks M v = 0.
-struct LayerReduceArgs {
-  const float* col;
-  int32_t units, d, mode;
-  float* vec;
-  float* n2;
-  float* n2_start;  // mode 0: ||v||^2 of the start vector
-  int32_t* lstat;
-};
-
-constexpr int kRedThreads = 512;
-
-__global__ void __launch_bounds__(kRedThreads) layer_reduce_kernel(LayerReduceArgs r) {
-  const int l = blockIdx.x, t = threadIdx.x;
-  __shared__ float red[kRedThreads / 64];
-  if (r.mode != 0 && r.lstat[l] != 0) return;
-  float acc = 0.f;
-  const float* base = r.col + (size_t)l * r.units * r.d;
-  for (int c = t; c < r.d; c += kRedThreads) {
-    float s = 0.f;
-    for (int u = 0; u < r.units; ++u) s += base[(size_t)u * r.d + c];
-    r.vec[(size_t)l * r.d + c] = s;
-    acc = fmaf(s, s, acc);
-  }
-  acc = wave_sum(acc);
-  if ((t & 63) == 0) red[t >> 6] = acc;
-  __syncthreads();
-  if (t == 0) {
-    const float n2 = sum_waves<kRedThreads / 64>(red);
-    r.n2[l] = n2;
-    if (r.mode == 0) {
-      r.n2_start[l] = n2;
-      r.lstat[l] = (n2 > 0.f && isfinite(n2)) ? 0 : -1;
-    } else if (r.mode == 1 && n2 == 0.f) {
-      r.lstat[l] = -2;
-    }
-  }
-}
-
-// Outputs of the layer-level form: sigma, scale, v = v'/||v'||, u = u'/sigma.
-struct LayerFinArgs {
-  int32_t d, L;
-  float coef;
-  const int32_t* lstat;
-  const float* lu;
-  const float* lv;
-  const float* n2_u;
-  const float* n2_v;
-  const float* n2_start;
-  float* v;
-  float* u;
-  float* sigma;
-  float* scale;
-};
-
-__global__ void __launch_bounds__(kThreads) layer_finalize_kernel(LayerFinArgs f) {
-  const int l = blockIdx.x;
-  const int st = f.lstat[l];
-  const float sig = st == -1 ? __builtin_nanf("") : st == -2 ? 0.f : sqrtf(f.n2_u[l]);
-  if (threadIdx.x == 0) {
-    f.sigma[l] = sig;
-    f.scale[l] = f.coef * sig;
-  }
-  float* vp = f.v + (size_t)l * f.d;
-  float* up = f.u ? f.u + (size_t)l * f.d : nullptr;
-  const float vs = st == 0 ? 1.0f / sqrtf(f.n2_v[l]) : st == -2 ? 1.0f / sqrtf(f.n2_start[l]) : 1.f;
-  const float us = st == 0 ? 1.0f / sig : 0.f;
-  for (int c = threadIdx.x; c < f.d; c += blockDim.x) {
-    if (st == 0) vp[c] = f.lv[(size_t)l * f.d + c] * vs;
-    else if (st == -2) vp[c] *= vs;
-    if (up) up[c] = st == 0 ? f.lu[(size_t)l * f.d + c] * us : 0.f;
-  }
-}
-
-// Normalises the final vectors and computes the per-layer scale.
-// Blocks [0, H): one head each; blocks [H, H + L): one layer each.
-__global__ void __launch_bounds__(kThreads) finalize_kernel(FinArgs f) {
-  const int b = blockIdx.x;
-  if (b < f.H) {
-    const int it = f.iters[b];
-    float vs = 1.f, us = 0.f;
-    bool touch_v = false;
-    if (it > 0) {
-      float n2 = 0.f;
-      const int slot = f.slot_fixed >= 0 ? f.slot_fixed : (it & 1);
-      for (int s = 0; s < f.s_k; ++s) n2 += f.w.zn[((size_t)slot * f.H + b) * f.s_k + s];
-      vs = 1.0f / sqrtf(n2);
-      us = 1.0f / f.sigma[b];
-      touch_v = true;
-    } else if (it == -2) {
-      vs = 1.0f / f.w.vnorm0[b];
-      touch_v = true;
-    }
-    float* vp = f.v + (size_t)b * f.d;
-    float* up = f.u ? f.u + (size_t)b * f.d : nullptr;
-    for (int c = threadIdx.x; c < f.d; c += blockDim.x) {
-      if (touch_v) vp[c] *= vs;
-      if (up) up[c] = (it > 0) ? up[c] * us : 0.f;
-    }
-  } else {
-    const int l = b - f.H;
-    __shared__ float red[kThreads];
-    __shared__ int nan_seen;
-    if (threadIdx.x == 0) nan_seen = 0;
-    __syncthreads();
-    float m = 0.f;
-    for (int h = threadIdx.x; h < f.n_q; h += blockDim.x) {
-      const float s = f.sigma[(size_t)l * f.n_q + h];
-      if (isnan(s)) nan_seen = 1;
-      m = fmaxf(m, s);
-    }
-    red[threadIdx.x] = m;
-    __syncthreads();
-    for (int off = kThreads / 2; off > 0; off >>= 1) {
-      if ((int)threadIdx.x < off) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + off]);
-      __syncthreads();
-    }
-    if (threadIdx.x == 0) f.scale[l] = nan_seen ? __builtin_nanf("") : f.coef * red[0];
-  }
-}
 
 // ------------------------------------------------------------------ host side
 
@@ -1484,56 +213,6 @@ hipEvent_t take_event(sn_ctx* c) {
   return e;
 }
 
-template <typename T, int DH, int GC>
-void launch_k(int ph, dim3 grid, hipStream_t st, const SweepArgs& a) {
-  if (ph == PH_INIT)
-    sweep_kernel<T, DH, GC, PH_INIT><<<grid, kThreads, 0, st>>>(a);
-  else if (ph == PH_K)
-    sweep_kernel<T, DH, GC, PH_K><<<grid, kThreads, 0, st>>>(a);
-  else if constexpr (DH >= 16)
-    sweep_kernel<T, DH, GC, PH_EK><<<grid, kThreads, 0, st>>>(a);
-}
-
-template <typename T, int DH>
-void launch_dh(int ph, int gc, bool mfma, dim3 grid, hipStream_t st, const SweepArgs& a) {
-  if (ph == PH_Q) {
-    sweep_kernel<T, DH, 1, PH_Q><<<grid, kThreads, 0, st>>>(a);
-    return;
-  }
-  if (ph == PH_EQ) {
-    if constexpr (DH >= 16) sweep_kernel<T, DH, 1, PH_EQ><<<grid, kThreads, 0, st>>>(a);
-    return;
-  }
-  if constexpr (std::is_same<T, uint16_t>::value && (DH == 64 || DH == 128)) {
-    if (mfma) {
-      const dim3 mgrid(ceil_div(a.n_items, kMWaves));
-      if (ph == PH_INIT)
-        ksweep_mfma_kernel<DH, PH_INIT><<<mgrid, 64 * kMWaves, 0, st>>>(a);
-      else if (ph == PH_K)
-        ksweep_mfma_kernel<DH, PH_K><<<mgrid, 64 * kMWaves, 0, st>>>(a);
-      else
-        ksweep_mfma_kernel<DH, PH_EK><<<mgrid, 64 * kMWaves, 0, st>>>(a);
-      return;
-    }
-  }
-  switch (gc) {
-    case 1: launch_k<T, DH, 1>(ph, grid, st, a); break;
-    case 2: launch_k<T, DH, 2>(ph, grid, st, a); break;
-    case 4: launch_k<T, DH, 4>(ph, grid, st, a); break;
-    default: launch_k<T, DH, 8>(ph, grid, st, a); break;
-  }
-}
-
-template <typename T>
-void launch_t(int dh, int ph, int gc, bool mfma, dim3 grid, hipStream_t st, const SweepArgs& a) {
-  switch (dh) {
-    case 8: launch_dh<T, 8>(ph, gc, mfma, grid, st, a); break;
-    case 16: launch_dh<T, 16>(ph, gc, mfma, grid, st, a); break;
-    case 32: launch_dh<T, 32>(ph, gc, mfma, grid, st, a); break;
-    case 64: launch_dh<T, 64>(ph, gc, mfma, grid, st, a); break;
-    default: launch_dh<T, 128>(ph, gc, mfma, grid, st, a); break;
-  }
-}
 
 // Brackets one launch with profiling events when profiling is on.
 template <typename F>
@@ -1554,7 +233,7 @@ int timed(sn_ctx* c, int kind, F&& launch) {
   return SN_OK;
 }
 
-int launch_sweep(sn_ctx* c, int ph, SweepArgs a) {
+int run_sweep(sn_ctx* c, int ph, SweepArgs a) {
   const Plan& pl = c->plan;
   if (ph == PH_Q || ph == PH_EQ) {
     a.mats = c->d_tab;
@@ -1569,25 +248,12 @@ int launch_sweep(sn_ctx* c, int ph, SweepArgs a) {
     a.n_tiles = pl.n_tiles;
     a.n_items = c->shape.n_layers * c->shape.n_kv_heads * pl.nch * pl.s_k;
   }
-  const dim3 grid(ceil_div(a.n_items, kWaves));
   const int kind = ph == PH_INIT ? KIND_INIT : ph == PH_Q ? KIND_Q : ph == PH_K ? KIND_K : KIND_EMIT;
   return timed(c, kind, [&] {
-    if (c->shape.dtype == SN_BF16)
-      launch_t<uint16_t>(c->shape.head_dim, ph, pl.gc, pl.mfma_k, grid, c->stream, a);
-    else
-      launch_t<float>(c->shape.head_dim, ph, pl.gc, pl.mfma_k, grid, c->stream, a);
+    launch_sweep(c->shape.dtype == SN_BF16, c->shape.head_dim, ph, pl.gc, pl.mfma_k, a.n_items, c->stream, a);
   });
 }
 
-template <typename T>
-void gram_dispatch(int dh, dim3 grid, hipStream_t st, const GramArgs& g) {
-  switch (dh) {
-    case 16: gram_kernel<T, 16><<<grid, 64 * kGWaves, 0, st>>>(g); break;
-    case 32: gram_kernel<T, 32><<<grid, 64 * kGWaves, 0, st>>>(g); break;
-    case 64: gram_kernel<T, 64><<<grid, 64 * kGWaves, 0, st>>>(g); break;
-    default: gram_kernel<T, 128><<<grid, 64 * kGWaves, 0, st>>>(g); break;
-  }
-}
 
 // Eq. "scale" per unit of sigma: alpha * d / sqrt(d_h) / (eta_fp8 * r_max), in double.
 float scale_coef(const sn_ctx* c) {
@@ -1623,16 +289,6 @@ int update_table(sn_ctx* c, const void* const* wq_layers, const void* const* wk_
   return SN_OK;
 }
 
-template <typename T, int MODE>
-void layer_dispatch(int dh, dim3 grid, hipStream_t st, const LayerArgs& a) {
-  switch (dh) {
-    case 8: layer_sweep_kernel<T, 8, MODE><<<grid, kThreads, 0, st>>>(a); break;
-    case 16: layer_sweep_kernel<T, 16, MODE><<<grid, kThreads, 0, st>>>(a); break;
-    case 32: layer_sweep_kernel<T, 32, MODE><<<grid, kThreads, 0, st>>>(a); break;
-    case 64: layer_sweep_kernel<T, 64, MODE><<<grid, kThreads, 0, st>>>(a); break;
-    default: layer_sweep_kernel<T, 128, MODE><<<grid, kThreads, 0, st>>>(a); break;
-  }
-}
 
 // One layer-form sweep over W_Q (q = true) or W_K.
 int layer_sweep(sn_ctx* c, bool q, int mode, LayerArgs a) {
@@ -1647,16 +303,8 @@ int layer_sweep(sn_ctx* c, bool q, int mode, LayerArgs a) {
   a.n_tiles = pl.n_tiles_q;
   a.n_items = L * a.units * a.s_out;
   a.lstat = reinterpret_cast<const int32_t*>(c->ws + pl.off_lstat);
-  const dim3 grid(ceil_div(a.n_items, kWaves));
-  const int dh = c->shape.head_dim;
   return timed(c, mode == LM_ROWS ? KIND_LROWS : KIND_LCOLS, [&] {
-    if (c->shape.dtype == SN_BF16) {
-      if (mode == LM_ROWS) layer_dispatch<uint16_t, LM_ROWS>(dh, grid, c->stream, a);
-      else layer_dispatch<uint16_t, LM_COLS>(dh, grid, c->stream, a);
-    } else {
-      if (mode == LM_ROWS) layer_dispatch<float, LM_ROWS>(dh, grid, c->stream, a);
-      else layer_dispatch<float, LM_COLS>(dh, grid, c->stream, a);
-    }
+    launch_layer_sweep(c->shape.dtype == SN_BF16, c->shape.head_dim, mode, a.n_items, c->stream, a);
   });
 }
 
@@ -1672,7 +320,7 @@ int layer_reduce(sn_ctx* c, const float* col, int units, int mode, float* vec, f
   r.n2_start = reinterpret_cast<float*>(c->ws + pl.off_ln2) + 2 * c->shape.n_layers;
   r.lstat = reinterpret_cast<int32_t*>(c->ws + pl.off_lstat);
   return timed(c, KIND_LRED,
-               [&] { layer_reduce_kernel<<<dim3(c->shape.n_layers), kRedThreads, 0, c->stream>>>(r); });
+               [&] { launch_layer_reduce(c->shape.n_layers, c->stream, r); });
 }
 
 // The sweeps of the default form: first W_K sweep, then n_iter x (W_Q sweep,
@@ -1681,14 +329,14 @@ int layer_reduce(sn_ctx* c, const float* col, int units, int mode, float* vec, f
 int run_chain(sn_ctx* c, SweepArgs a, float* u) {
   int rc;
   a.k = 0;
-  if ((rc = launch_sweep(c, PH_INIT, a)) != SN_OK) return rc;
+  if ((rc = run_sweep(c, PH_INIT, a)) != SN_OK) return rc;
   int next_check = 2;
   for (int k = 1; k <= a.n_iter; ++k) {
     a.k = k;
     a.want_vec = (u != nullptr) && (c->params.tol > 0.f || k == a.n_iter);
-    if ((rc = launch_sweep(c, PH_Q, a)) != SN_OK) return rc;
+    if ((rc = run_sweep(c, PH_Q, a)) != SN_OK) return rc;
     a.want_vec = 0;
-    if ((rc = launch_sweep(c, PH_K, a)) != SN_OK) return rc;
+    if ((rc = run_sweep(c, PH_K, a)) != SN_OK) return rc;
     if (c->params.tol > 0.f && k == next_check && k < a.n_iter) {
       SN_HIP(hipMemcpyAsync(c->h_alive, c->w.n_alive + (k & 1), sizeof(int32_t), hipMemcpyDeviceToHost,
                             c->stream));
@@ -1706,7 +354,7 @@ int run_gram(sn_ctx* c, SweepArgs a, float* u) {
   const Plan& pl = c->plan;
   int rc;
   a.k = 0;
-  if ((rc = launch_sweep(c, PH_INIT, a)) != SN_OK) return rc;
+  if ((rc = run_sweep(c, PH_INIT, a)) != SN_OK) return rc;
 
   GramArgs g{};
   g.mats = c->d_tab;
@@ -1721,14 +369,8 @@ int run_gram(sn_ctx* c, SweepArgs a, float* u) {
   g.n_tiles = pl.n_tiles_g;
   g.n_items = pl.units_g * pl.s_g;
   g.gp = reinterpret_cast<float*>(c->ws + pl.off_gp);
-  const dim3 ggrid(ceil_div(g.n_items, kGWaves));
   const int dh = c->shape.head_dim;
-  rc = timed(c, KIND_GRAM, [&] {
-    if (c->shape.dtype == SN_BF16)
-      gram_dispatch<uint16_t>(dh, ggrid, c->stream, g);
-    else
-      gram_dispatch<float>(dh, ggrid, c->stream, g);
-  });
+  rc = timed(c, KIND_GRAM, [&] { launch_gram(c->shape.dtype == SN_BF16, dh, g.n_items, c->stream, g); });
   if (rc != SN_OK) return rc;
 
   IterArgs it{};
@@ -1744,19 +386,12 @@ int run_gram(sn_ctx* c, SweepArgs a, float* u) {
   it.w = c->w;
   it.sigma = a.sigma;
   it.iters = a.iters;
-  rc = timed(c, KIND_ITER, [&] {
-    switch (dh) {
-      case 16: gram_iterate_kernel<16><<<dim3(pl.H), IterShape<16>::NT, 0, c->stream>>>(it); break;
-      case 32: gram_iterate_kernel<32><<<dim3(pl.H), IterShape<32>::NT, 0, c->stream>>>(it); break;
-      case 64: gram_iterate_kernel<64><<<dim3(pl.H), IterShape<64>::NT, 0, c->stream>>>(it); break;
-      default: gram_iterate_kernel<128><<<dim3(pl.H), IterShape<128>::NT, 0, c->stream>>>(it); break;
-    }
-  });
+  rc = timed(c, KIND_ITER, [&] { launch_gram_iterate(dh, pl.H, c->stream, it); });
   if (rc != SN_OK) return rc;
 
   a.k = 0;  // the final sweeps write their ||v'||^2 partials to slot 0
-  if ((rc = launch_sweep(c, PH_EK, a)) != SN_OK) return rc;
-  if (u && (rc = launch_sweep(c, PH_EQ, a)) != SN_OK) return rc;
+  if ((rc = run_sweep(c, PH_EK, a)) != SN_OK) return rc;
+  if (u && (rc = run_sweep(c, PH_EQ, a)) != SN_OK) return rc;
   return SN_OK;
 }
 
@@ -1909,7 +544,7 @@ SN_API int spectral_step(sn_ctx* c, const void* const* wq_layers, const void* co
   f.sigma = sigma;
   f.scale = scale;
   f.iters = a.iters;
-  return timed(c, KIND_FIN, [&] { finalize_kernel<<<dim3(pl.H + L), kThreads, 0, c->stream>>>(f); });
+  return timed(c, KIND_FIN, [&] { launch_finalize(pl.H + L, c->stream, f); });
 }
 
 SN_API int spectral_step_layer(sn_ctx* c, const void* const* wq_layers, const void* const* wk_layers, float* v,
@@ -1976,7 +611,7 @@ SN_API int spectral_step_layer(sn_ctx* c, const void* const* wq_layers, const vo
   f.u = u;
   f.sigma = sigma;
   f.scale = scale;
-  return timed(c, KIND_LRED, [&] { layer_finalize_kernel<<<dim3(L), kThreads, 0, c->stream>>>(f); });
+  return timed(c, KIND_LRED, [&] { launch_layer_finalize(L, c->stream, f); });
 }
 
 SN_API int spectral_logits_workspace_bytes(const sn_shape* shape, int32_t seq_len, int64_t* bytes) {

@@ -25,7 +25,7 @@ struct LogitArgs {
   const uint16_t* ql;
   const uint16_t* kh;
   const uint16_t* kl;
-  int32_t seq, g, nq_cols, nk_cols, tiles;
+  int32_t seq, g, nq_cols, nk_cols, tiles, n_heads;
   const float* scale;  // device [L]
   int32_t layer;
   uint8_t* codes;      // [n_q][seq][seq] of this layer, or nullptr
@@ -36,4 +36,4 @@ struct LogitArgs {
 int64_t sn_logits_workspace_bytes(int64_t seq, int64_t nq_cols, int64_t nk_cols);
 void sn_launch_zero_stats(float* max_abs, int32_t* n_over, int n, hipStream_t st);
 void sn_launch_proj(const ProjArgs& a, hipStream_t st);
-void sn_launch_logits(const LogitArgs& a, int head_dim, int n_q, hipStream_t st);
+void sn_launch_logits(const LogitArgs& a, int head_dim, hipStream_t st);

@@ -145,62 +145,93 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs a) {
 }
 
 // Logits of one layer: one 128 x 128 tile of S for one query head per
-// workgroup, 64 x 64 per wave, contraction over d_h in steps of 32.  The
-// products are formed transposed (A = key rows, B = query rows), so a lane
-// holds 4 consecutive columns of one row of S: one 32-bit word of E4M3
-// codes.  v_cvt_pk_fp8_f32 (no clamp) rounds to nearest even and gives the
-// NaN code past 464, the OCP E4M3FN conversion the oracle defines; a
-// bit-by-bit comparison with an integer encoder over every rounding point
-// and 400k random values in [-600, 600] found no difference for non-NaN
-// inputs.
+// workgroup, 64 x 64 per wave.  The workgroup stages the hi and lo planes of
+// its 128 query rows and 128 key rows through LDS, 64 columns of d_h at a
+// time (coalesced loads; see stage_issue), and every wave reads its operands
+// back in the MFMA layout.  The products are formed transposed (A = key
+// rows, B = query rows), so a lane holds 4 consecutive columns of one row of
+// S: one 32-bit word of E4M3 codes.  v_cvt_pk_fp8_f32 (no clamp) rounds to
+// nearest even and gives the NaN code past 464, the OCP E4M3FN conversion the
+// oracle defines; a bit-by-bit comparison with an integer encoder over every
+// rounding point and 400k random values in [-600, 600] found no difference
+// for non-NaN inputs.
+constexpr int kPlaneBytes = kTile * 128;  // 128 rows x 64 columns of one bf16 plane
+
 template <int DH>
 __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
-  constexpr int KC = (DH + 31) / 32;
+  constexpr int NSTEP = (DH + 63) / 64;  // 64-column steps over d_h
+  __shared__ __attribute__((aligned(16))) uint8_t stage[4 * kPlaneBytes];  // Q hi, Q lo, K hi, K lo
   const int lane = threadIdx.x & 63;
   const int wv = uni((int)(threadIdx.x >> 6));
   const int q = lane >> 4, s = lane & 15;
+  // consecutive tiles (one head after another, the heads of a key group in
+  // turn) run on one XCD and share its L2
   const int per_head = a.tiles * a.tiles;
-  const int h = blockIdx.x / per_head;
-  const int ti = (blockIdx.x % per_head) / a.tiles, tj = blockIdx.x % a.tiles;
-  const int i0 = ti * kTile + (wv >> 1) * 64, j0 = tj * kTile + (wv & 1) * 64;
-  if (i0 >= a.seq || j0 >= a.seq) return;
+  const int per_xcd = gridDim.x / 8;
+  const int b = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (b >= a.n_heads * per_head) return;  // whole workgroup
+  const int h = b / per_head;
+  const int ti = (b % per_head) / a.tiles, tj = b % a.tiles;
   const int kvh = h / a.g;
+  const int wm = wv >> 1, wn = wv & 1;
+  const int i0 = ti * kTile + 64 * wm, j0 = tj * kTile + 64 * wn;  // this wave's rows of S
 
-  const int64_t qrow = (int64_t)a.nq_cols * 2, krow = (int64_t)a.nk_cols * 2;
-  const uint32_t q_bytes = (uint32_t)((((int64_t)(a.seq - 1 - i0) * a.nq_cols + DH) * 2 + 15) & ~int64_t(15));
-  const uint32_t k_bytes = (uint32_t)((((int64_t)(a.seq - 1 - j0) * a.nk_cols + DH) * 2 + 15) & ~int64_t(15));
-  const size_t qo = (size_t)i0 * a.nq_cols + (size_t)h * DH, ko = (size_t)j0 * a.nk_cols + (size_t)kvh * DH;
-  const __amdgpu_buffer_rsrc_t rqh = make_rsrc(a.qh + qo, q_bytes), rql = make_rsrc(a.ql + qo, q_bytes);
-  const __amdgpu_buffer_rsrc_t rkh = make_rsrc(a.kh + ko, k_bytes), rkl = make_rsrc(a.kl + ko, k_bytes);
-  const uint32_t q_off = (uint32_t)(s * qrow + 16 * q), k_off = (uint32_t)(s * krow + 16 * q);
-  const uint32_t q16 = (uint32_t)(16 * qrow), k16 = (uint32_t)(16 * krow);
+  // this wave stages rows 32 wv .. 32 wv + 31 of the four planes
+  const int qr = ti * kTile + 32 * wv, kr = tj * kTile + 32 * wv;
+  const int64_t q_len = qr < a.seq ? (((int64_t)(a.seq - 1 - qr) * a.nq_cols + DH) * 2 + 15) & ~int64_t(15) : 0;
+  const int64_t k_len = kr < a.seq ? (((int64_t)(a.seq - 1 - kr) * a.nk_cols + DH) * 2 + 15) & ~int64_t(15) : 0;
+  const size_t qo = (size_t)qr * a.nq_cols + (size_t)h * DH, ko = (size_t)kr * a.nk_cols + (size_t)kvh * DH;
+  const __amdgpu_buffer_rsrc_t rqh = make_rsrc(a.qh + qo, (uint32_t)q_len), rql = make_rsrc(a.ql + qo, (uint32_t)q_len);
+  const __amdgpu_buffer_rsrc_t rkh = make_rsrc(a.kh + ko, (uint32_t)k_len), rkl = make_rsrc(a.kl + ko, (uint32_t)k_len);
+  const uint32_t q_rb = (uint32_t)(a.nq_cols * 2), k_rb = (uint32_t)(a.nk_cols * 2);
+  auto issue = [&](int st) {
+    const uint32_t col = (uint32_t)(st * 128);
+    stage_issue<32, 0>(rqh, stage + 0 * kPlaneBytes + 4096 * wv, col, q_rb, lane);
+    stage_issue<32, 0>(rql, stage + 1 * kPlaneBytes + 4096 * wv, col, q_rb, lane);
+    stage_issue<32, 0>(rkh, stage + 2 * kPlaneBytes + 4096 * wv, col, k_rb, lane);
+    stage_issue<32, 0>(rkl, stage + 3 * kPlaneBytes + 4096 * wv, col, k_rb, lane);
+  };
 
   f32x4 acc[4][4];  // acc[i][j][e] = S[i0 + 16 i + s][j0 + 16 j + 4 q + e]
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  issue(0);
 #pragma unroll
-  for (int kc = 0; kc < KC; ++kc) {
-    const bool kval = 32 * kc + 8 * q < DH;  // chunks past d_h belong to the next head
-    u32x4 ah[4], al[4], bh[4], bl[4];
+  for (int st = 0; st < NSTEP; ++st) {
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's part of step st is in LDS
+    __syncthreads();                // every part
+    u32x4 ah[2][4], al[2][4], bh[2][4], bl[2][4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      ah[r] = __builtin_amdgcn_raw_buffer_load_b128(rqh, q_off + 64 * kc, r * q16, 0);
-      al[r] = __builtin_amdgcn_raw_buffer_load_b128(rql, q_off + 64 * kc, r * q16, 0);
-      bh[r] = __builtin_amdgcn_raw_buffer_load_b128(rkh, k_off + 64 * kc, r * k16, 0);
-      bl[r] = __builtin_amdgcn_raw_buffer_load_b128(rkl, k_off + 64 * kc, r * k16, 0);
-      if (!kval) ah[r] = al[r] = bh[r] = bl[r] = u32x4{0u, 0u, 0u, 0u};
+    for (int kc = 0; kc < 2; ++kc) {
+      const bool kval = st * 64 + 32 * kc + 8 * q < DH;  // chunks past d_h belong to the next head
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        ah[kc][r] = stage_chunk(stage + 0 * kPlaneBytes, 64 * wm + 16 * r + s, 4 * kc + q);
+        al[kc][r] = stage_chunk(stage + 1 * kPlaneBytes, 64 * wm + 16 * r + s, 4 * kc + q);
+        bh[kc][r] = stage_chunk(stage + 2 * kPlaneBytes, 64 * wn + 16 * r + s, 4 * kc + q);
+        bl[kc][r] = stage_chunk(stage + 3 * kPlaneBytes, 64 * wn + 16 * r + s, 4 * kc + q);
+        if (!kval) ah[kc][r] = al[kc][r] = bh[kc][r] = bl[kc][r] = u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+    if (st + 1 < NSTEP) {
+      __builtin_amdgcn_s_waitcnt(0);  // read out
+      __syncthreads();                // by every wave, before the next step overwrites
+      issue(st + 1);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        acc[i][j] = mfma(bh[j], ah[i], acc[i][j]);
-        acc[i][j] = mfma(bl[j], ah[i], acc[i][j]);
-        acc[i][j] = mfma(bh[j], al[i], acc[i][j]);
-      }
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          acc[i][j] = mfma(bh[kc][j], ah[kc][i], acc[i][j]);
+          acc[i][j] = mfma(bl[kc][j], ah[kc][i], acc[i][j]);
+          acc[i][j] = mfma(bh[kc][j], al[kc][i], acc[i][j]);
+        }
   }
+  if (i0 >= a.seq || j0 >= a.seq) return;
 
   // S~ = (q . k) / (sqrt(d_h) scale), the factor formed in double
   const float c = (float)(1.0 / (std::sqrt((double)DH) * (double)a.scale[a.layer]));
@@ -272,8 +303,8 @@ void sn_launch_proj(const ProjArgs& a, hipStream_t st) {
   proj_kernel<<<dim3(((tiles + 7) / 8) * 8), 64 * kWaves, 0, st>>>(a);
 }
 
-void sn_launch_logits(const LogitArgs& a, int head_dim, int n_q, hipStream_t st) {
-  const dim3 grid(n_q * a.tiles * a.tiles);
+void sn_launch_logits(const LogitArgs& a, int head_dim, hipStream_t st) {
+  const dim3 grid(((a.n_heads * a.tiles * a.tiles + 7) / 8) * 8);
   switch (head_dim) {
     case 16: logits_kernel<16><<<grid, 64 * kWaves, 0, st>>>(a); break;
     case 32: logits_kernel<32><<<grid, 64 * kWaves, 0, st>>>(a); break;

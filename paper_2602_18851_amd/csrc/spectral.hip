@@ -680,6 +680,7 @@ SN_API int spectral_logits_fp8(sn_ctx* c, const void* const* x_layers, int64_t l
   g.nq_cols = (int32_t)nq_cols;
   g.nk_cols = (int32_t)nk_cols;
   g.tiles = ceil_div(seq_len, 128);
+  g.n_heads = sh.n_q_heads;
   g.scale = scale;
   int rc = timed(c, KIND_LOGITS, [&] { sn_launch_zero_stats(max_abs, n_over, L * sh.n_q_heads, c->stream); });
   if (rc != SN_OK) return rc;
@@ -692,7 +693,7 @@ SN_API int spectral_logits_fp8(sn_ctx* c, const void* const* x_layers, int64_t l
     g.codes = codes ? codes + (size_t)l * sh.n_q_heads * seq_len * seq_len : nullptr;
     g.max_abs = max_abs + (size_t)l * sh.n_q_heads;
     g.n_over = n_over + (size_t)l * sh.n_q_heads;
-    if ((rc = timed(c, KIND_LOGITS, [&] { sn_launch_logits(g, dh, sh.n_q_heads, c->stream); })) != SN_OK)
+    if ((rc = timed(c, KIND_LOGITS, [&] { sn_launch_logits(g, dh, c->stream); })) != SN_OK)
       return rc;
   }
   return SN_OK;

@@ -180,8 +180,10 @@ SN_API int spectral_step_layer(sn_ctx* ctx, const void* const* wq_layers, const 
  * relative precision (three bf16 matrix-core products on hi/lo halves).
  * Needs bf16 weights and tokens and head_dim 16, 32, 64 or 128.
  *
- * spectral_logits_workspace_bytes: device scratch the call needs
- * (seq_len * (n_q + n_kv) * head_dim * 4 bytes; it holds one layer's Q, K).
+ * spectral_logits_workspace_bytes: device scratch the call needs: a table
+ * of 3 n_layers device pointers (padded to 256 bytes), then the Q and K of
+ * every layer as hi and lo bf16 planes (n_layers * seq_len * (n_q + n_kv) *
+ * head_dim * 4 bytes).  One launch of each kernel covers all layers.
  *
  * spectral_logits_fp8:
  *   x_layers   host array of n_layers device pointers: tokens of layer l,
@@ -195,6 +197,9 @@ SN_API int spectral_step_layer(sn_ctx* ctx, const void* const* wq_layers, const 
  *   max_abs    device float32 [n_layers][n_q]: max |S~| per head.
  *   n_over     device int32 [n_layers][n_q]: #{(i, j): |S~_ij| > 448}.
  * Queued on the context's stream; allocates nothing; seq_len <= 46340.
+ * The layer pointer table is copied into the workspace from host memory
+ * with hipMemcpyAsync (staged before the call returns), so the call is not
+ * meant for stream capture.
  * Errors: SN_ENULL, SN_EINVAL, SN_EDTYPE, SN_ESTATE. */
 SN_API int spectral_logits_workspace_bytes(const sn_shape* shape, int32_t seq_len, int64_t* bytes);
 SN_API int spectral_logits_fp8(sn_ctx* ctx, const void* const* x_layers, int64_t ld_x, int32_t seq_len,

@@ -45,9 +45,9 @@ __device__ __forceinline__ void mask_bf16(u32x4& q, int nval) {
 
 __device__ __forceinline__ uint16_t bf16_bits(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
 
-// Q and K projections of one layer.  Tiles of 128 tokens x 128 output
-// features, Q features first, then K; a wave covers 64 x 64 (4 x 4 blocks of
-// 16 x 16).  The workgroup streams the 128 token rows and 128 weight rows of
+// Q and K projections of all layers in one launch.  Tiles of 128 tokens x
+// 128 output features, per layer Q features first, then K; a wave covers
+// 64 x 64 (4 x 4 blocks of 16 x 16).  The workgroup streams the 128 token rows and 128 weight rows of
 // its tile through LDS in steps of 64 columns (128-byte row segments, coalesced
 // loads straight to LDS, two stages; see stage_issue), and every wave reads
 // its operands back in the MFMA layout.  Workgroups are numbered so that the
@@ -61,9 +61,10 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs a) {
   const int wv = uni((int)(threadIdx.x >> 6));
   const int q = lane >> 4, s = lane & 15;
   const int per_xcd = gridDim.x / 8;
-  const int t = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  const int tiles_q = a.tiles_m * a.tiles_nq;
-  if (t >= tiles_q + a.tiles_m * a.tiles_nk) return;  // whole workgroup
+  const int tq = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  const int tiles_q = a.tiles_m * a.tiles_nq, per_layer = tiles_q + a.tiles_m * a.tiles_nk;
+  if (tq >= a.layers * per_layer) return;  // whole workgroup
+  const int layer = tq / per_layer, t = tq % per_layer;
   const bool isq = t < tiles_q;
   const int tt = isq ? t : t - tiles_q;
   const int bm = tt % a.tiles_m, bn = tt / a.tiles_m;
@@ -71,8 +72,8 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs a) {
 
   // this wave stages rows 32 wv .. 32 wv + 31 of the A (token) and B (weight) tiles
   const int am = bm * kTile + 32 * wv, bnr = bn * kTile + 32 * wv;
-  const char* abase = reinterpret_cast<const char*>(a.x) + (int64_t)am * a.ld_x * 2;
-  const char* bbase = reinterpret_cast<const char*>(isq ? a.wq : a.wk) + (int64_t)bnr * a.ld_w * 2;
+  const char* abase = uni(a.x[layer]) + (int64_t)am * a.ld_x * 2;
+  const char* bbase = uni(isq ? a.wq[layer] : a.wk[layer]) + (int64_t)bnr * a.ld_w * 2;
   const int64_t a_len = am < a.seq ? (((int64_t)(a.seq - 1 - am) * a.ld_x + a.d) * 2 + 15) & ~int64_t(15) : 0;
   const int64_t b_len = bnr < ncols ? (((int64_t)(ncols - 1 - bnr) * a.ld_w + a.d) * 2 + 15) & ~int64_t(15) : 0;
   const __amdgpu_buffer_rsrc_t ra = make_rsrc(abase, (uint32_t)a_len);
@@ -126,8 +127,9 @@ __global__ void __launch_bounds__(64 * kWaves) proj_kernel(ProjArgs a) {
   }
 
   const int m0 = bm * kTile + 64 * wm, n0 = bn * kTile + 64 * wn;
-  uint16_t* hi = isq ? a.qh : a.kh;
-  uint16_t* lo = isq ? a.ql : a.kl;
+  const size_t plane = (size_t)layer * a.seq * ncols;
+  uint16_t* hi = (isq ? a.qh : a.kh) + plane;
+  uint16_t* lo = (isq ? a.ql : a.kl) + plane;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -168,8 +170,9 @@ __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
   // turn) run on one XCD and share its L2
   const int per_head = a.tiles * a.tiles;
   const int per_xcd = gridDim.x / 8;
-  const int b = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (b >= a.n_heads * per_head) return;  // whole workgroup
+  const int bl = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  if (bl >= a.layers * a.n_heads * per_head) return;  // whole workgroup
+  const int layer = bl / (a.n_heads * per_head), b = bl % (a.n_heads * per_head);
   const int h = b / per_head;
   const int ti = (b % per_head) / a.tiles, tj = b % a.tiles;
   const int kvh = h / a.g;
@@ -180,7 +183,8 @@ __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
   const int qr = ti * kTile + 32 * wv, kr = tj * kTile + 32 * wv;
   const int64_t q_len = qr < a.seq ? (((int64_t)(a.seq - 1 - qr) * a.nq_cols + DH) * 2 + 15) & ~int64_t(15) : 0;
   const int64_t k_len = kr < a.seq ? (((int64_t)(a.seq - 1 - kr) * a.nk_cols + DH) * 2 + 15) & ~int64_t(15) : 0;
-  const size_t qo = (size_t)qr * a.nq_cols + (size_t)h * DH, ko = (size_t)kr * a.nk_cols + (size_t)kvh * DH;
+  const size_t qo = ((size_t)layer * a.seq + qr) * a.nq_cols + (size_t)h * DH;
+  const size_t ko = ((size_t)layer * a.seq + kr) * a.nk_cols + (size_t)kvh * DH;
   const __amdgpu_buffer_rsrc_t rqh = make_rsrc(a.qh + qo, (uint32_t)q_len), rql = make_rsrc(a.ql + qo, (uint32_t)q_len);
   const __amdgpu_buffer_rsrc_t rkh = make_rsrc(a.kh + ko, (uint32_t)k_len), rkl = make_rsrc(a.kl + ko, (uint32_t)k_len);
   const uint32_t q_rb = (uint32_t)(a.nq_cols * 2), k_rb = (uint32_t)(a.nk_cols * 2);
@@ -234,7 +238,7 @@ __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
   if (i0 >= a.seq || j0 >= a.seq) return;
 
   // S~ = (q . k) / (sqrt(d_h) scale), the factor formed in double
-  const float c = (float)(1.0 / (std::sqrt((double)DH) * (double)a.scale[a.layer]));
+  const float c = (float)(1.0 / (std::sqrt((double)DH) * (double)a.scale[layer]));
   const bool words = (a.seq & 3) == 0;  // rows start 4-byte aligned
   int n_over = 0;
   float mx = 0.f;
@@ -256,7 +260,7 @@ __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
       if (a.codes && row < a.seq) {
         int w = __builtin_amdgcn_cvt_pk_fp8_f32(v[0], v[1], 0, false);
         w = __builtin_amdgcn_cvt_pk_fp8_f32(v[2], v[3], w, true);
-        uint8_t* out = a.codes + ((size_t)h * a.seq + row) * a.seq + col;
+        uint8_t* out = a.codes + (((size_t)layer * a.n_heads + h) * a.seq + row) * a.seq + col;
         if (words && col + 3 < a.seq) {
           *reinterpret_cast<int*>(out) = w;
         } else {
@@ -275,8 +279,9 @@ __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
     mx = fmaxf(mx, __shfl_xor(mx, m));
   }
   if (lane == 0) {
-    if (n_over) atomicAdd(a.n_over + h, n_over);
-    atomicMax(reinterpret_cast<int32_t*>(a.max_abs) + h, __float_as_int(mx));
+    const int hl = layer * a.n_heads + h;
+    if (n_over) atomicAdd(a.n_over + hl, n_over);
+    atomicMax(reinterpret_cast<int32_t*>(a.max_abs) + hl, __float_as_int(mx));
   }
 }
 
@@ -290,8 +295,10 @@ __global__ void zero_stats_kernel(float* max_abs, int32_t* n_over, int n) {
 
 }  // namespace
 
-int64_t sn_logits_workspace_bytes(int64_t seq, int64_t nq_cols, int64_t nk_cols) {
-  return seq * (nq_cols + nk_cols) * 4;  // hi and lo bf16 planes of Q and K
+int64_t sn_logits_workspace_bytes(int64_t layers, int64_t seq, int64_t nq_cols, int64_t nk_cols) {
+  // device pointer tables (tokens, wq, wk of every layer), then the hi and lo
+  // bf16 planes of Q and K of every layer
+  return ((3 * layers * 8 + 255) & ~int64_t(255)) + layers * seq * (nq_cols + nk_cols) * 4;
 }
 
 void sn_launch_zero_stats(float* max_abs, int32_t* n_over, int n, hipStream_t st) {
@@ -299,12 +306,12 @@ void sn_launch_zero_stats(float* max_abs, int32_t* n_over, int n, hipStream_t st
 }
 
 void sn_launch_proj(const ProjArgs& a, hipStream_t st) {
-  const int tiles = a.tiles_m * (a.tiles_nq + a.tiles_nk);
+  const int tiles = a.layers * a.tiles_m * (a.tiles_nq + a.tiles_nk);
   proj_kernel<<<dim3(((tiles + 7) / 8) * 8), 64 * kWaves, 0, st>>>(a);
 }
 
 void sn_launch_logits(const LogitArgs& a, int head_dim, hipStream_t st) {
-  const dim3 grid(((a.n_heads * a.tiles * a.tiles + 7) / 8) * 8);
+  const dim3 grid(((a.layers * a.n_heads * a.tiles * a.tiles + 7) / 8) * 8);
   switch (head_dim) {
     case 16: logits_kernel<16><<<grid, 64 * kWaves, 0, st>>>(a); break;
     case 32: logits_kernel<32><<<grid, 64 * kWaves, 0, st>>>(a); break;

@@ -617,7 +617,8 @@ SN_API int spectral_step_layer(sn_ctx* c, const void* const* wq_layers, const vo
 SN_API int spectral_logits_workspace_bytes(const sn_shape* shape, int32_t seq_len, int64_t* bytes) {
   if (!shape || !bytes) return fail(SN_ENULL, "shape and bytes must not be NULL");
   if (seq_len < 1) return fail(SN_EINVAL, "seq_len must be >= 1");
-  *bytes = sn_logits_workspace_bytes(seq_len, (int64_t)shape->n_q_heads * shape->head_dim,
+  if (shape->n_layers < 1) return fail(SN_EINVAL, "n_layers must be >= 1");
+  *bytes = sn_logits_workspace_bytes(shape->n_layers, seq_len, (int64_t)shape->n_q_heads * shape->head_dim,
                                      (int64_t)shape->n_kv_heads * shape->head_dim);
   return SN_OK;
 }
@@ -637,28 +638,45 @@ SN_API int spectral_logits_fp8(sn_ctx* c, const void* const* x_layers, int64_t l
   if (seq_len < 1 || seq_len > 46340) return fail(SN_EINVAL, "seq_len must be in [1, 46340]");
   if (ld_x == 0) ld_x = sh.d_model;
   if (ld_x < sh.d_model || (ld_x * 2) % 16 != 0) return fail(SN_EINVAL, "ld_x must be >= d_model, 8-element aligned");
+  const int L = sh.n_layers;
   const int64_t nq_cols = (int64_t)sh.n_q_heads * dh, nk_cols = (int64_t)sh.n_kv_heads * dh;
   if ((int64_t)seq_len * ld_x * 2 >= (int64_t(1) << 31) || (int64_t)seq_len * nq_cols * 2 >= (int64_t(1) << 31))
     return fail(SN_EINVAL, "seq_len x row bytes must stay below 2^31");
-  const int64_t need = sn_logits_workspace_bytes(seq_len, nq_cols, nk_cols);
+  const int64_t tiles = ceil_div(seq_len, 128);
+  if ((int64_t)L * sh.n_q_heads * tiles * tiles >= (int64_t(1) << 31) ||
+      (int64_t)L * tiles * ceil_div(nq_cols + nk_cols, 128) >= (int64_t(1) << 31))
+    return fail(SN_EINVAL, "n_layers x n_q x (seq_len / 128)^2 must stay below 2^31");
+  const int64_t need = sn_logits_workspace_bytes(L, seq_len, nq_cols, nk_cols);
   if (workspace_bytes < need) return fail(SN_EINVAL, "workspace too small (spectral_logits_workspace_bytes)");
   if ((reinterpret_cast<uintptr_t>(workspace) & 255) || (reinterpret_cast<uintptr_t>(codes) & 15))
     return fail(SN_EINVAL, "workspace must be 256-byte and codes 16-byte aligned");
-  const int L = sh.n_layers;
+  std::vector<const void*> tab(3 * (size_t)L);
   for (int l = 0; l < L; ++l) {
     if (!x_layers[l] || !wq_layers[l] || !wk_layers[l]) return fail(SN_ENULL, "a layer pointer is NULL");
     if ((reinterpret_cast<uintptr_t>(x_layers[l]) | reinterpret_cast<uintptr_t>(wq_layers[l]) |
          reinterpret_cast<uintptr_t>(wk_layers[l])) & 15)
       return fail(SN_EINVAL, "layer pointers must be 16-byte aligned");
+    tab[l] = x_layers[l];
+    tab[L + l] = wq_layers[l];
+    tab[2 * L + l] = wk_layers[l];
   }
   int cur_dev = 0;
   SN_HIP(hipGetDevice(&cur_dev));
   if (cur_dev != c->device) return fail(SN_ESTATE, "the current HIP device is not the context's device");
 
-  uint16_t* ws = reinterpret_cast<uint16_t*>(workspace);
+  // pointer tables at the start of the workspace (copied from pageable host
+  // memory: the runtime stages it before the call returns)
+  const void** d_tab = reinterpret_cast<const void**>(workspace);
+  SN_HIP(hipMemcpyAsync(d_tab, tab.data(), tab.size() * sizeof(void*), hipMemcpyHostToDevice, c->stream));
+  uint16_t* planes = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(workspace) + ((3 * L * 8 + 255) & ~255));
+  const size_t qn = (size_t)L * seq_len * nq_cols, kn = (size_t)L * seq_len * nk_cols;
   ProjArgs p{};
+  p.x = d_tab;
+  p.wq = d_tab + L;
+  p.wk = d_tab + 2 * L;
   p.ld_x = ld_x;
   p.ld_w = sh.ld;
+  p.layers = L;
   p.seq = seq_len;
   p.d = sh.d_model;
   p.nq_cols = (int32_t)nq_cols;
@@ -666,15 +684,16 @@ SN_API int spectral_logits_fp8(sn_ctx* c, const void* const* x_layers, int64_t l
   p.tiles_m = ceil_div(seq_len, 128);
   p.tiles_nq = ceil_div(nq_cols, 128);
   p.tiles_nk = ceil_div(nk_cols, 128);
-  p.qh = ws;
-  p.ql = ws + (size_t)seq_len * nq_cols;
-  p.kh = ws + (size_t)2 * seq_len * nq_cols;
-  p.kl = p.kh + (size_t)seq_len * nk_cols;
+  p.qh = planes;
+  p.ql = planes + qn;
+  p.kh = planes + 2 * qn;
+  p.kl = planes + 2 * qn + kn;
   LogitArgs g{};
   g.qh = p.qh;
   g.ql = p.ql;
   g.kh = p.kh;
   g.kl = p.kl;
+  g.layers = L;
   g.seq = seq_len;
   g.g = c->plan.g;
   g.nq_cols = (int32_t)nq_cols;
@@ -682,21 +701,12 @@ SN_API int spectral_logits_fp8(sn_ctx* c, const void* const* x_layers, int64_t l
   g.tiles = ceil_div(seq_len, 128);
   g.n_heads = sh.n_q_heads;
   g.scale = scale;
+  g.codes = codes;
+  g.max_abs = max_abs;
+  g.n_over = n_over;
   int rc = timed(c, KIND_LOGITS, [&] { sn_launch_zero_stats(max_abs, n_over, L * sh.n_q_heads, c->stream); });
   if (rc != SN_OK) return rc;
-  for (int l = 0; l < L; ++l) {
-    p.x = reinterpret_cast<const uint16_t*>(x_layers[l]);
-    p.wq = reinterpret_cast<const uint16_t*>(wq_layers[l]);
-    p.wk = reinterpret_cast<const uint16_t*>(wk_layers[l]);
-    if ((rc = timed(c, KIND_PROJ, [&] { sn_launch_proj(p, c->stream); })) != SN_OK) return rc;
-    g.layer = l;
-    g.codes = codes ? codes + (size_t)l * sh.n_q_heads * seq_len * seq_len : nullptr;
-    g.max_abs = max_abs + (size_t)l * sh.n_q_heads;
-    g.n_over = n_over + (size_t)l * sh.n_q_heads;
-    if ((rc = timed(c, KIND_LOGITS, [&] { sn_launch_logits(g, dh, c->stream); })) != SN_OK)
-      return rc;
-  }
-  return SN_OK;
+  if ((rc = timed(c, KIND_PROJ, [&] { sn_launch_proj(p, c->stream); })) != SN_OK) return rc;
+  return timed(c, KIND_LOGITS, [&] { sn_launch_logits(g, dh, c->stream); });
 }
-
 }  // extern "C"

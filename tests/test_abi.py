@@ -117,3 +117,14 @@ def test_layer_form_needs_its_flag(lib):
     # column buffer of every query head plus u', v' per layer
     assert lay - base >= (2 * 8 * 256 + 2 * 2 * 256) * 4
     assert lib.spectral_step_layer(None, None, None, None, None, 1, None, None) == sp.SN_ENULL
+
+
+def test_logit_consumer_workspace_holds_every_layer(lib):
+    # pointer table of 3 L device pointers padded to 256 bytes, then hi/lo
+    # bf16 planes of Q (n_q d_h columns) and K (n_kv d_h columns) per layer
+    for L, seq in ((2, 100), (80, 1024)):
+        got = sp.spectral_logits_workspace_bytes(_shape(n_layers=L), seq)
+        table = (3 * L * 8 + 255) // 256 * 256
+        assert got == table + L * seq * (8 + 2) * 64 * 4
+    with pytest.raises(sp.SpectralError):
+        sp.spectral_logits_workspace_bytes(_shape(), 0)

@@ -251,11 +251,11 @@ def bench_fp8(args):
                      for l in range(wl.n_layers)]).to(dev)
     est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, flags=SN_FLAG_GRAM)
     _, scale, _ = est.step(wq, wk, start_vectors(wl, dev), wl.n_iter)   # the layer scales the consumer uses
-    ws = torch.empty(seq * (wl.n_q + wl.n_kv) * wl.head_dim * 4, dtype=torch.uint8, device=dev)
+    from paper_2602_18851_amd.spectral import spectral_logits_fp8, spectral_logits_workspace_bytes
+    ws = torch.empty(spectral_logits_workspace_bytes(est.shape, seq), dtype=torch.uint8, device=dev)
     codes = torch.empty(wl.n_layers, wl.n_q, seq, seq, dtype=torch.uint8, device=dev)
 
     # the timed call writes the codes; buffers are allocated once, outside it
-    from paper_2602_18851_amd.spectral import spectral_logits_fp8
     max_abs = torch.empty(wl.n_layers, wl.n_q, dtype=torch.float32, device=dev)
     n_over = torch.empty(wl.n_layers, wl.n_q, dtype=torch.int32, device=dev)
     xs = [t.data_ptr() for t in x.unbind(0)]
@@ -284,8 +284,9 @@ def bench_fp8(args):
     est.profile(False)
     p_ms, p_n = prof["logits_projection"]
     l_ms, l_n = prof["logits_fp8"]
-    proj_flops = 2.0 * seq * wl.d_model * (wl.n_q + wl.n_kv) * wl.head_dim   # per launch (one layer)
-    logit_flops = 3 * 2.0 * seq * seq * wl.head_dim * wl.n_q                  # per launch, three bf16 products
+    # one launch of each kernel covers every layer
+    proj_flops = 2.0 * seq * wl.d_model * (wl.n_q + wl.n_kv) * wl.head_dim * wl.n_layers
+    logit_flops = 3 * 2.0 * seq * seq * wl.head_dim * wl.n_q * wl.n_layers   # three bf16 products
     tflops = proj_flops / (p_ms / p_n * 1e-3) / 1e12
     logits = wl.n_layers * wl.n_q * seq * seq
     out = {

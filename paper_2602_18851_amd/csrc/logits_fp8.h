@@ -14,7 +14,7 @@ struct ProjArgs {
   const void* const* wk;  // device table [L]: [n_kv d_h][ld_w] bf16
   int64_t ld_w;
   int32_t layers, seq, d, nq_cols, nk_cols;  // nq_cols = n_q d_h, nk_cols = n_kv d_h
-  int32_t tiles_m, tiles_nq, tiles_nk;       // per layer
+  int32_t tiles_m, tiles_nq, tiles_nk;       // per layer (set by sn_launch_proj)
   uint16_t* qh;  // [L][seq][nq_cols] bf16 planes: Q = hi + lo
   uint16_t* ql;
   uint16_t* kh;  // [L][seq][nk_cols]

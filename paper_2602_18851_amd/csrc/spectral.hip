@@ -681,9 +681,6 @@ SN_API int spectral_logits_fp8(sn_ctx* c, const void* const* x_layers, int64_t l
   p.d = sh.d_model;
   p.nq_cols = (int32_t)nq_cols;
   p.nk_cols = (int32_t)nk_cols;
-  p.tiles_m = ceil_div(seq_len, 128);
-  p.tiles_nq = ceil_div(nq_cols, 128);
-  p.tiles_nk = ceil_div(nk_cols, 128);
   p.qh = planes;
   p.ql = planes + qn;
   p.kh = planes + 2 * qn;

@@ -73,11 +73,17 @@ gram_kernel(GramArgs a) {
   const int t0 = strip * a.tps;
   const int t1 = min(t0 + a.tps, a.n_tiles);
 
-  // one LDS tile per wave: tile t + 1 streams in while tile t is multiplied
-  // from registers
-  if (t0 < t1) stage_issue<DH, kStreamPolicy>(rsrc, tile, (uint32_t)(t0 * 128), row_bytes, lane);
+  // one LDS tile per wave: the next tile streams in while this one is
+  // multiplied from registers.  Each wave starts at its own pseudo-random
+  // tile of the strip and wraps around, so that side-by-side waves read
+  // different column offsets of their strided rows.
+  const int n_mine = t1 - t0;
+  const int rot = n_mine > 1 ? (int)((((uint32_t)item * 2654435761u) >> 16) % (uint32_t)n_mine) : 0;
+  auto tile_at = [&](int i) { const int u = rot + i; return t0 + (u >= n_mine ? u - n_mine : u); };
+  if (n_mine > 0) stage_issue<DH, kStreamPolicy>(rsrc, tile, (uint32_t)(tile_at(0) * 128), row_bytes, lane);
 #pragma unroll 1
-  for (int t = t0; t < t1; ++t) {
+  for (int i = 0; i < n_mine; ++i) {
+    const int t = tile_at(i);
     __builtin_amdgcn_s_waitcnt(0);  // the tile is in LDS
     u32x4 fr[RB][2];
 #pragma unroll
@@ -85,7 +91,7 @@ gram_kernel(GramArgs a) {
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc) fr[rb][kc] = stage_chunk(tile, 16 * rb + s, 4 * kc + q);
     __builtin_amdgcn_s_waitcnt(0);  // read out before the next tile overwrites it
-    if (t + 1 < t1) stage_issue<DH, kStreamPolicy>(rsrc, tile, (uint32_t)((t + 1) * 128), row_bytes, lane);
+    if (i + 1 < n_mine) stage_issue<DH, kStreamPolicy>(rsrc, tile, (uint32_t)(tile_at(i + 1) * 128), row_bytes, lane);
     if (t >= n_full) {  // the ragged last tile: zero columns >= d
 #pragma unroll
       for (int kc = 0; kc < 2; ++kc) {

@@ -76,13 +76,18 @@ layer_sweep_kernel(LayerArgs a) {
   const int n_full = a.d / TILE_C;
   const int t0 = strip * a.tps;
   const int t1 = min(t0 + a.tps, a.n_tiles);
+  // staggered start tile and loads ahead of arithmetic, as in the W_Q sweep
+  const int n_mine = t1 - t0;
+  int t = t0;
+  if (n_mine > 1) t += (int)(((uint32_t)item * 2654435761u) >> 16) % n_mine;
 #pragma unroll 1
-  for (int t = t0; t < t1; ++t) {
+  for (int i = 0; i < n_mine; ++i, t = (t + 1 == t1) ? t0 : t + 1) {
     u32x4 tile[RPL];
     const uint32_t voff = lane_off + (uint32_t)(t * TILE_C * ES);
 #pragma unroll
     for (int rr = 0; rr < RPL; ++rr)
       tile[rr] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, rr * row_bytes, kStreamPolicy);
+    __builtin_amdgcn_sched_barrier(0);
     const int col = t * TILE_C + chunk * VEC;
     const int nval = a.d - col;  // >= VEC on full tiles
     if (t >= n_full) {

@@ -472,10 +472,17 @@ ksweep_mfma_kernel(SweepArgs a) {
   const int t1 = min(t0 + a.tps, a.n_tiles);  // exclusive
   uint16_t* vl = &lds_v[wv][0];
 
+  // staggered start tile, as in the W_Q sweep
+  const int n_mine = t1 - t0;
+  const int rot = n_mine > 1
+                      ? (int)((((uint32_t)(blockIdx.x * kMWaves + wv) * 2654435761u) >> 16) % (uint32_t)n_mine)
+                      : 0;
+  auto tile_at = [&](int i) { const int u = rot + i; return t0 + (u >= n_mine ? u - n_mine : u); };
   __builtin_amdgcn_s_waitcnt(0);  // xs is read out before the first tile overwrites it
-  if (t0 < t1) stage_issue<DH, kStreamPolicy>(rsrc, tl, (uint32_t)(t0 * 128), row_bytes, lane);
+  if (n_mine > 0) stage_issue<DH, kStreamPolicy>(rsrc, tl, (uint32_t)(tile_at(0) * 128), row_bytes, lane);
 #pragma unroll 1
-  for (int t = t0; t < t1; ++t) {
+  for (int i = 0; i < n_mine; ++i) {
+    const int t = tile_at(i);
     const int c0 = t * kMTileC;
     __builtin_amdgcn_s_waitcnt(0);  // tile t is in LDS
     f32x4 d1[CB];
@@ -497,7 +504,7 @@ ksweep_mfma_kernel(SweepArgs a) {
         for (int kc = 0; kc < KC; ++kc) cur[rb][kc] = stage_chunk(tl, 16 * rb + s, 4 * kc + g);
     }
     __builtin_amdgcn_s_waitcnt(0);  // the tile is read out: stage the next one
-    if (t + 1 < t1) stage_issue<DH, kStreamPolicy>(rsrc, tl, (uint32_t)((t + 1) * 128), row_bytes, lane);
+    if (i + 1 < n_mine) stage_issue<DH, kStreamPolicy>(rsrc, tl, (uint32_t)(tile_at(i + 1) * 128), row_bytes, lane);
     if (PROD2 && t >= n_full) {  // the ragged last tile: zero columns >= d
 #pragma unroll
       for (int kc = 0; kc < KC; ++kc) {

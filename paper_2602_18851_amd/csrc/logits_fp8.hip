@@ -46,19 +46,20 @@ __device__ __forceinline__ void mask_bf16(u32x4& q, int nval) {
 __device__ __forceinline__ uint16_t bf16_bits(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
 
 // Q and K projections of all layers in one launch.  Workgroup tiles of
-// 256 tokens x 256 output features (per layer Q features first, then K); each
-// of the 4 waves covers 128 x 128 as 8 x 8 blocks of 16 x 16, so a wave's
-// accumulators fill the accumulation registers and every operand chunk read
-// from LDS feeds 8 matrix-core products.  The workgroup streams its 256 token
-// rows and 256 weight rows through LDS in steps of 64 columns (128-byte row
-// segments, coalesced loads straight to LDS, two stages of 64 KB; see
-// stage_issue).  Workgroups are numbered so that the consecutive token tiles
-// of one feature tile run on one XCD (the hardware deals workgroups
-// round-robin over the 8 XCDs) and share its L2.
+// 256 tokens x 256 output features (per layer Q features first, then K) and
+// 8 waves, two per SIMD, each covering 128 x 64 as 8 x 4 blocks of 16 x 16:
+// while one wave of a SIMD waits for LDS or the barrier, the other keeps the
+// matrix core busy.  The workgroup streams its 256 token rows and 256 weight
+// rows through LDS in steps of 64 columns (128-byte row segments, coalesced
+// loads straight to LDS, two stages of 64 KB; see stage_issue).  Workgroups
+// are numbered so that the consecutive token tiles of one feature tile run on
+// one XCD (the hardware deals workgroups round-robin over the 8 XCDs) and
+// share its L2.
 constexpr int kPT = 256;                    // projection workgroup tile
+constexpr int kPWaves = 8;
 constexpr int kPStageBytes = 2 * kPT * 128;  // A and B rows of one 64-column step
 
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) proj_kernel(ProjArgs a) {
+__global__ void __launch_bounds__(64 * kPWaves) __attribute__((amdgpu_waves_per_eu(2, 2))) proj_kernel(ProjArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t stage[2][kPStageBytes];
   const int lane = threadIdx.x & 63;
   const int wv = uni((int)(threadIdx.x >> 6));
@@ -73,8 +74,8 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
   const int bm = tt % a.tiles_m, bn = tt / a.tiles_m;
   const int ncols = isq ? a.nq_cols : a.nk_cols;
 
-  // this wave stages rows 64 wv .. 64 wv + 63 of the A (token) and B (weight) tiles
-  const int am = bm * kPT + 64 * wv, bnr = bn * kPT + 64 * wv;
+  // this wave stages rows 32 wv .. 32 wv + 31 of the A (token) and B (weight) tiles
+  const int am = bm * kPT + 32 * wv, bnr = bn * kPT + 32 * wv;
   const char* abase = uni(a.x[layer]) + (int64_t)am * a.ld_x * 2;
   const char* bbase = uni(isq ? a.wq[layer] : a.wk[layer]) + (int64_t)bnr * a.ld_w * 2;
   const int64_t a_len = am < a.seq ? (((int64_t)(a.seq - 1 - am) * a.ld_x + a.d) * 2 + 15) & ~int64_t(15) : 0;
@@ -83,16 +84,16 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
   const __amdgpu_buffer_rsrc_t rb_ = make_rsrc(bbase, (uint32_t)b_len);
   const uint32_t a_rb = (uint32_t)(a.ld_x * 2), b_rb = (uint32_t)(a.ld_w * 2);
   auto issue = [&](int k, int st) {
-    stage_issue<64, 0>(ra, stage[st] + 8192 * wv, (uint32_t)(k * 128), a_rb, lane);
-    stage_issue<64, 0>(rb_, stage[st] + kPT * 128 + 8192 * wv, (uint32_t)(k * 128), b_rb, lane);
+    stage_issue<32, 0>(ra, stage[st] + 4096 * wv, (uint32_t)(k * 128), a_rb, lane);
+    stage_issue<32, 0>(rb_, stage[st] + kPT * 128 + 4096 * wv, (uint32_t)(k * 128), b_rb, lane);
   };
 
-  const int wm = wv >> 1, wn = wv & 1;
-  f32x4 acc[8][8];
+  const int wm = wv >> 2, wn = wv & 3;  // 2 x 4 waves of 128 x 64
+  f32x4 acc[8][4];
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int n_k = (a.d + 63) / 64, n_full = a.d / 64;
   issue(0, 0);
 #pragma unroll 1
@@ -104,35 +105,33 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))
     const uint8_t* sb = sa + kPT * 128;
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc) {
-      u32x4 fa[8], fb[8];
+      u32x4 fa[8], fb[4];
 #pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        fa[r] = stage_chunk(sa, 128 * wm + 16 * r + s, 4 * kc + q);
-        fb[r] = stage_chunk(sb, 128 * wn + 16 * r + s, 4 * kc + q);
-      }
+      for (int r = 0; r < 8; ++r) fa[r] = stage_chunk(sa, 128 * wm + 16 * r + s, 4 * kc + q);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) fb[r] = stage_chunk(sb, 64 * wn + 16 * r + s, 4 * kc + q);
       if (k >= n_full) {  // the ragged last step: zero columns >= d
         const int nval = a.d - (k * 64 + 32 * kc + 8 * q);
 #pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          mask_bf16(fa[r], nval);
-          mask_bf16(fb[r], nval);
-        }
+        for (int r = 0; r < 8; ++r) mask_bf16(fa[r], nval);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) mask_bf16(fb[r], nval);
       }
 #pragma unroll
       for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc[i][j] = mfma(fa[i], fb[j], acc[i][j]);
+        for (int j = 0; j < 4; ++j) acc[i][j] = mfma(fa[i], fb[j], acc[i][j]);
     }
   }
 
-  const int m0 = bm * kPT + 128 * wm, n0 = bn * kPT + 128 * wn;
+  const int m0 = bm * kPT + 128 * wm, n0 = bn * kPT + 64 * wn;
   const size_t plane = (size_t)layer * a.seq * ncols;
   uint16_t* hi = (isq ? a.qh : a.kh) + plane;
   uint16_t* lo = (isq ? a.ql : a.kl) + plane;
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int m = m0 + 16 * i + 4 * q + e, n = n0 + 16 * j + s;
@@ -310,7 +309,7 @@ void sn_launch_proj(const ProjArgs& args, hipStream_t st) {
   a.tiles_nq = (a.nq_cols + kPT - 1) / kPT;
   a.tiles_nk = (a.nk_cols + kPT - 1) / kPT;
   const int tiles = a.layers * a.tiles_m * (a.tiles_nq + a.tiles_nk);
-  proj_kernel<<<dim3(((tiles + 7) / 8) * 8), 256, 0, st>>>(a);
+  proj_kernel<<<dim3(((tiles + 7) / 8) * 8), 64 * kPWaves, 0, st>>>(a);
 }
 
 void sn_launch_logits(const LogitArgs& a, int head_dim, hipStream_t st) {

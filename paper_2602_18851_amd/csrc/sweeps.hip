@@ -77,18 +77,45 @@ __device__ __forceinline__ Item decode_item(const SweepArgs& a, int item) {
 // the W_Q sweep), status / sigma / iteration outputs (written once, by the
 // strip-0 wave), and the normalised input vector of every active head, summed
 // over the producer's strips in a fixed order, into xs[i][0 .. d_h).
+// The per-head scalars are gathered by lanes 0 .. nvalid - 1 in one round of
+// loads and the partial vectors of all heads in s_in rounds, instead of a
+// chain of dependent loads per head.
+__device__ __forceinline__ float lane_f(float x, int i) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), i));
+}
+
 template <int DH, int GC, int PH>
 __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, int lane, float (*xs)[DH],
                                            bool (&act)[GC], bool (&last)[GC]) {
   const int strip = itm.strip, head0 = itm.head0, nvalid = itm.nvalid;
   const int slot_prev = (a.k + 1) & 1;  // parity of step k-1
   const int slot_cur = a.k & 1;
-  // ---- per-head decisions (wave-uniform) and normalised input vectors
+  constexpr bool ITER = PH == PH_Q || PH == PH_K;
+  // ---- per-head scalars: lane i reads head head0 + i
+  int l_alive = 0;
+  float l_nv2 = 0.f, l_n2 = 0.f, l_s2 = 0.f, l_prev = 0.f;
+  if (ITER && lane < nvalid) {
+    const int hh = head0 + lane;
+    l_alive = a.w.alive[slot_prev * a.H + hh];
+    if (a.k == 1)
+      for (int s = 0; s < a.s_k; ++s) l_nv2 += a.w.zn[hh * a.s_k + s];
+    if (PH == PH_Q) {
+      for (int s = 0; s < a.s_k; ++s) l_n2 += a.w.zn[(slot_prev * a.H + hh) * a.s_k + s];
+    } else {
+      for (int s = 0; s < a.s_q; ++s) l_s2 += a.w.yn[hh * a.s_q + s];
+      l_prev = a.w.sig[slot_prev * a.H + hh];
+    }
+  }
+  // ---- per-head decisions (wave-uniform)
   int n_cont = 0;
+  float inv[GC];
+  const float* part[GC];
 #pragma unroll
   for (int i = 0; i < GC; ++i) {
     act[i] = false;
     last[i] = false;
+    inv[i] = 0.f;
+    part[i] = nullptr;
     if (i >= nvalid) continue;
     const int hh = head0 + i;
     if (PH == PH_INIT) {
@@ -105,46 +132,36 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
       }
       continue;
     }
-    bool alive = uni(a.w.alive[slot_prev * a.H + hh]) != 0;
+    bool alive = __builtin_amdgcn_readlane(l_alive, i) != 0;
     bool dead_v = false, dead_m = false;
     float nv2 = 0.f;
     if (a.k == 1) {
-      for (int s = 0; s < a.s_k; ++s) nv2 += a.w.zn[hh * a.s_k + s];
-      nv2 = uni(nv2);
+      nv2 = lane_f(l_nv2, i);
       if (!(nv2 > 0.f) || !isfinite(nv2)) {
         alive = false;
         dead_v = true;
       }
     }
-    float inv = 0.f;
-    const float* part = nullptr;
-    int s_in = 0;
     if (PH == PH_Q) {
       if (alive) {
-        float n2 = 0.f;
-        for (int s = 0; s < a.s_k; ++s) n2 += a.w.zn[(slot_prev * a.H + hh) * a.s_k + s];
-        inv = 1.0f / sqrtf(uni(n2));
-        part = a.w.zp + ((size_t)slot_prev * a.H + hh) * a.s_k * DH;
-        s_in = a.s_k;
+        inv[i] = 1.0f / sqrtf(lane_f(l_n2, i));
+        part[i] = a.w.zp + ((size_t)slot_prev * a.H + hh) * a.s_k * DH;
         act[i] = true;
       }
     } else {  // PH_K: sigma of this step is now complete
       float sigma = 0.f;
       if (alive) {
-        float s2 = 0.f;
-        for (int s = 0; s < a.s_q; ++s) s2 += a.w.yn[hh * a.s_q + s];
-        s2 = uni(s2);
+        const float s2 = lane_f(l_s2, i);
         sigma = sqrtf(s2);
         if (s2 == 0.f) {
           dead_m = true;
         } else {
           act[i] = true;
-          const float prev = uni(a.w.sig[slot_prev * a.H + hh]);
+          const float prev = lane_f(l_prev, i);
           last[i] = (a.k >= a.n_iter) ||
                     (a.tol > 0.f && a.k >= 2 && fabsf(sigma - prev) <= a.tol * sigma);
-          inv = 1.0f / sigma;
-          part = a.w.yp + (size_t)hh * a.s_q * DH;
-          s_in = a.s_q;
+          inv[i] = 1.0f / sigma;
+          part[i] = a.w.yp + (size_t)hh * a.s_q * DH;
         }
       }
       if (strip == 0 && lane == 0) {
@@ -169,15 +186,38 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
       n_cont += (act[i] && !last[i]) ? 1 : 0;
     }
     if (PH == PH_Q && dead_v) act[i] = false;
-    if (act[i]) {
-      for (int r = lane; r < DH; r += 64) {
-        float s = 0.f;
-        for (int t = 0; t < s_in; ++t) s += part[t * DH + r];
-        xs[i][r] = s * inv;
+  }
+  if (PH == PH_K && strip == 0 && lane == 0 && n_cont > 0) atomicAdd(&a.w.n_alive[slot_cur], n_cont);
+  if (!ITER) return;
+
+  // ---- normalised input vectors: partial t of every active head, t = 0, 1, ...
+  constexpr int NR = (DH + 63) / 64;
+  const int s_in = PH == PH_Q ? a.s_k : a.s_q;
+  float xv[GC][NR];
+#pragma unroll
+  for (int i = 0; i < GC; ++i)
+#pragma unroll
+    for (int rr = 0; rr < NR; ++rr) xv[i][rr] = 0.f;
+  for (int t = 0; t < s_in; ++t) {
+#pragma unroll
+    for (int i = 0; i < GC; ++i) {
+      if (!act[i]) continue;
+#pragma unroll
+      for (int rr = 0; rr < NR; ++rr) {
+        const int r = lane + 64 * rr;
+        if (r < DH) xv[i][rr] += part[i][t * DH + r];
       }
     }
   }
-  if (PH == PH_K && strip == 0 && lane == 0 && n_cont > 0) atomicAdd(&a.w.n_alive[slot_cur], n_cont);
+#pragma unroll
+  for (int i = 0; i < GC; ++i) {
+    if (!act[i]) continue;
+#pragma unroll
+    for (int rr = 0; rr < NR; ++rr) {
+      const int r = lane + 64 * rr;
+      if (r < DH) xs[i][r] = xv[i][rr] * inv[i];
+    }
+  }
 }
 
 template <typename T, int DH, int GC, int PH>

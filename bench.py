@@ -36,8 +36,9 @@ KERNEL_DIR = os.path.join(ROOT, "paper_2602_18851_amd", "csrc")
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=10)
-    p.add_argument("--warmup", type=int, default=3)
+    # the warm-up and timed-call counts of the paper's protocol (App. "Overhead Measurement")
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", default="llama2-70b-gqa")
     p.add_argument("--n-iter", type=int, default=0, help="override the workload's iteration count")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle CPU baseline")

@@ -146,3 +146,43 @@ def test_full_size_70b_sampled_heads():
     print(f"70B: max |S~| over all heads {max_abs.max().item():.1f}, overflowing heads "
           f"{int((n_over > 0).sum())} of {n_over.numel()}")
     est.close()
+
+
+def test_separate_layer_buffers_and_several_row_tiles():
+    """Layers passed as separately allocated tensors (the device pointer table
+    then holds unrelated addresses) give the same bits as one stacked tensor,
+    and both match the oracle; 520 tokens span three 256-row projection tiles
+    and five 128-row logit tiles, the last ones ragged."""
+    wl = WORKLOADS["llama2-70b-gqa"].replace(key="sep-layers", std=0.02, n_layers=3, d_model=320, n_q=4, n_kv=2,
+                                              head_dim=64)
+    seq = 520
+    wq, wk = all_weights(wl, "cpu")
+    xs = [layer_tokens(wl, seq, l) for l in range(wl.n_layers)]
+    scales = []
+    for l in range(wl.n_layers):
+        m = max(np.abs(fp8_consumer.head_logits(xs[l].double().numpy(), wq[l].double().numpy(),
+                                                wk[l].double().numpy(), h, wl.n_kv, wl.head_dim)).max()
+                for h in range(wl.n_q))
+        scales.append(m / 500.0)
+    scale_dev = torch.tensor(scales, dtype=torch.float32, device="cuda")
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha)
+    stacked = est.logits_fp8(torch.stack(xs).cuda(), wq.cuda(), wk.cuda(), scale_dev, want_codes=True)
+    # separate allocations in reverse layer order, with gaps between them
+    keep, x_l, q_l, k_l = [], [None] * wl.n_layers, [None] * wl.n_layers, [None] * wl.n_layers
+    for l in reversed(range(wl.n_layers)):
+        x_l[l] = xs[l].cuda()
+        keep.append(torch.empty(4097, dtype=torch.uint8, device="cuda"))
+        q_l[l] = wq[l].clone().cuda()
+        k_l[l] = wk[l].clone().cuda()
+    sep = est.logits_fp8(x_l, q_l, k_l, scale_dev, want_codes=True)
+    torch.cuda.synchronize()
+    for a_, b_ in zip(stacked, sep):
+        np.testing.assert_array_equal(a_.cpu().numpy(), b_.cpu().numpy())
+    max_abs, n_over, codes = (t.cpu().numpy() for t in sep)
+    s32 = scale_dev.cpu().double().numpy()
+    for l in range(wl.n_layers):
+        for h in range(wl.n_q):
+            check_head(codes[l, h], max_abs[l, h], n_over[l, h], xs[l], wq[l], wk[l], s32[l], h, wl.n_kv,
+                       wl.head_dim)
+    assert n_over.sum() > 0
+    est.close()

@@ -5,7 +5,8 @@
 // overflow when |S| > scale * R_max; Table "pretrained": largest scaled
 // logit; App. "FP8 Utilization Statistics").
 //
-// For one layer with tokens X (seq x d, bf16):
+// For each layer, with that layer's tokens X (seq x d, bf16); one launch of
+// each kernel covers every layer:
 //   Q = X W_Q^T, K = X W_K^T                 (projection GEMMs, fp32 accumulation)
 //   S_h = Q_h K_{j(h)}^T / sqrt(d_h)        (j(h) = floor(h / g), no key expansion)
 //   S~_h = S_h / scale                       -> OCP E4M3FN code, round to nearest even;
@@ -28,7 +29,7 @@ namespace {
 
 using namespace sn_dev;
 
-constexpr int kWaves = 4;      // 2 x 2 waves of 64 x 64 per 128 x 128 workgroup tile
+constexpr int kWaves = 4;      // logit kernel: 2 x 2 waves of 64 x 64 per 128 x 128 tile
 constexpr int kTile = 128;
 
 __device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, const f32x4& c) {
@@ -144,8 +145,8 @@ __global__ void __launch_bounds__(64 * kPWaves) __attribute__((amdgpu_waves_per_
       }
 }
 
-// Logits of one layer: one 128 x 128 tile of S for one query head per
-// workgroup, 64 x 64 per wave.  The workgroup stages the hi and lo planes of
+// Logits of all layers in one launch: one 128 x 128 tile of S of one query
+// head of one layer per workgroup, 64 x 64 per wave.  The workgroup stages the hi and lo planes of
 // its 128 query rows and 128 key rows through LDS, 64 columns of d_h at a
 // time (coalesced loads; see stage_issue), and every wave reads its operands
 // back in the MFMA layout.  The products are formed transposed (A = key

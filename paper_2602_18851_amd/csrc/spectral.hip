@@ -97,10 +97,13 @@ int validate(const sn_shape* s, const sn_params* p) {
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 // Column strips per unit (head or KV head): the request if given, else about
-// target / units (rounded up, or down when all waves should be resident at once).
+// target / units (rounded up, or down when all waves should be resident at
+// once), with at least kMinTilesPerStrip tiles per strip so that a wave's
+// stream outweighs its prologue (which sums one partial per producer strip).
 void strips(int n_tiles, int64_t units, int requested, int target, bool round_down, int* s_out, int* tps_out) {
   const int64_t u = std::max<int64_t>(units, 1);
   int s = requested > 0 ? requested : round_down ? (int)std::max<int64_t>(1, target / u) : ceil_div(target, u);
+  if (requested <= 0) s = std::min(s, std::max(1, n_tiles / kMinTilesPerStrip));
   s = std::max(1, std::min(s, n_tiles));
   const int tps = ceil_div(n_tiles, s);
   *tps_out = tps;

@@ -198,6 +198,7 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
   for (int i = 0; i < GC; ++i)
 #pragma unroll
     for (int rr = 0; rr < NR; ++rr) xv[i][rr] = 0.f;
+#pragma unroll 4
   for (int t = 0; t < s_in; ++t) {
 #pragma unroll
     for (int i = 0; i < GC; ++i) {
@@ -239,14 +240,6 @@ sweep_kernel(SweepArgs a) {
   const Item itm = decode_item<DH, GC, PH>(a, blockIdx.x * kWaves + wv);
   const int layer = itm.layer, row0 = itm.row0, head0 = itm.head0, strip = itm.strip;
   const int slot_cur = a.k & 1;
-  bool act[GC], last[GC];
-  head_setup<DH, GC, PH>(a, itm, lane, xs[wv], act, last);
-  __syncthreads();
-
-  bool any = false;
-#pragma unroll
-  for (int i = 0; i < GC; ++i) any |= act[i];
-  if (!any) return;
 
   // Buffer resource over this head's (or KV head's) d_h x ld row block; the
   // hardware range check returns zeros past the last valid element, and the
@@ -261,6 +254,40 @@ sweep_kernel(SweepArgs a) {
       __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(blk), (short)0, (int)nrec, kRsrcWord3);
   const uint32_t lane_off = (uint32_t)(((int64_t)rg * RPL * a.ld + chunk * VEC) * ES);
   const uint32_t row_bytes = (uint32_t)(a.ld * ES);
+  auto load_tile = [&](u32x4 (&tile)[RPL], int t) {
+    const uint32_t voff = lane_off + (uint32_t)(t * TILE_C * ES);
+#pragma unroll
+    for (int rr = 0; rr < RPL; ++rr)
+      tile[rr] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, rr * row_bytes, kStreamPolicy);
+  };
+
+  const int n_full = a.d / TILE_C;  // tiles whose columns are all inside d
+  const int t_first = strip * a.tps;
+  const int t_last = min(t_first + a.tps, a.n_tiles);  // exclusive
+  const int t_full_end = min(t_last, n_full);
+  const bool has_tail = t_last > n_full;               // the ragged last tile is ours
+  // Each wave starts at its own pseudo-random tile of the strip and wraps
+  // around, so the waves that run side by side read different column
+  // offsets of their 16 KB-strided rows rather than the same ones in
+  // lockstep; and all loads of a tile are issued before any of its
+  // arithmetic.  Together with two strips per head this took the 70B W_Q
+  // sweep from 6.56 to 6.78 TB/s.  The first tile is requested before the
+  // per-head set-up below, whose loads it does not depend on, so the two
+  // latencies overlap.
+  const int n_mine = itm.nvalid > 0 ? t_full_end - t_first : 0;
+  int t = t_first;
+  if (n_mine > 1) t += (int)(((uint32_t)(blockIdx.x * kWaves + wv) * 2654435761u) >> 16) % n_mine;
+  u32x4 first[RPL];
+  if (n_mine > 0) load_tile(first, t);
+
+  bool act[GC], last[GC];
+  head_setup<DH, GC, PH>(a, itm, lane, xs[wv], act, last);
+  __syncthreads();
+
+  bool any = false;
+#pragma unroll
+  for (int i = 0; i < GC; ++i) any |= act[i];
+  if (!any) return;
 
   float xr1[GC == 1 ? RPL : 1];
   if (GC == 1 && PH != PH_INIT) {
@@ -277,18 +304,6 @@ sweep_kernel(SweepArgs a) {
     for (int rr = 0; rr < RPL; ++rr) acc[i][rr] = 0.f;
   }
 
-  const int n_full = a.d / TILE_C;  // tiles whose columns are all inside d
-  const int t_first = strip * a.tps;
-  const int t_last = min(t_first + a.tps, a.n_tiles);  // exclusive
-  const int t_full_end = min(t_last, n_full);
-  const bool has_tail = t_last > n_full;               // the ragged last tile is ours
-
-  auto load_tile = [&](u32x4 (&tile)[RPL], int t) {
-    const uint32_t voff = lane_off + (uint32_t)(t * TILE_C * ES);
-#pragma unroll
-    for (int rr = 0; rr < RPL; ++rr)
-      tile[rr] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff, rr * row_bytes, kStreamPolicy);
-  };
   auto tile_step = [&](auto full_tag, int t, u32x4 (&tile)[RPL]) {
     constexpr bool FULL = decltype(full_tag)::value;
     const int col = t * TILE_C + chunk * VEC;
@@ -358,17 +373,12 @@ sweep_kernel(SweepArgs a) {
     }
   };
 
-  // Each wave starts at its own pseudo-random tile of the strip and wraps
-  // around, so the waves that run side by side read different column
-  // offsets of their 16 KB-strided rows rather than the same ones in
-  // lockstep; and all loads of a tile are issued before any of its
-  // arithmetic.  Together with two strips per head this took the 70B W_Q
-  // sweep from 6.56 to 6.78 TB/s.
-  const int n_mine = t_full_end - t_first;
-  int t = t_first;
-  if (n_mine > 1) t += (int)(((uint32_t)(blockIdx.x * kWaves + wv) * 2654435761u) >> 16) % n_mine;
+  if (n_mine > 0) {
+    tile_step(std::true_type{}, t, first);
+    if (++t == t_full_end) t = t_first;
+  }
 #pragma unroll 1
-  for (int i = 0; i < n_mine; ++i) {
+  for (int i = 1; i < n_mine; ++i) {
     u32x4 cur[RPL];
     load_tile(cur, t);
     __builtin_amdgcn_sched_barrier(0);

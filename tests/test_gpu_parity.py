@@ -357,3 +357,33 @@ def test_full_size_per_step_recompute(form):
     print(f"per-step: {len(heads)} heads ({matched} compared on both calls), max rel err {worst:.3e}, "
           f"iters {it.min()}..{it.max()} (median {np.median(it)})")
     est.close()
+
+
+def _random_cases(n=16, seed=20260218):
+    """Seeded random small shapes: MHA and GQA (1 to 12 query heads per key
+    head), d_h 8..128, fp32 and bf16, ragged widths with padded rows,
+    automatic or forced strip counts, 1..12 iterations."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        dt = str(rng.choice(["f32", "bf16"]))
+        align = 4 if dt == "f32" else 8  # 16-byte rows
+        d = int(rng.integers(8, 1300))
+        ld = -(-d // align) * align + align * int(rng.integers(0, 3))
+        over = dict(n_layers=int(rng.integers(1, 4)), d_model=d, n_kv=int(rng.integers(1, 4)),
+                    head_dim=int(rng.choice([8, 16, 32, 64, 128])), dtype=dt)
+        over["n_q"] = over["n_kv"] * int(rng.choice([1, 2, 3, 4, 8, 12]))
+        strips = {} if rng.random() < 0.5 else dict(q_strips=int(rng.integers(1, 7)), k_strips=int(rng.integers(1, 7)))
+        cases.append((f"rand{i}-{dt}-d{d}-ld{ld}-q{over['n_q']}kv{over['n_kv']}-dh{over['head_dim']}", 100 + i,
+                      over, ld, strips, int(rng.integers(1, 13))))
+    return cases
+
+
+@pytest.mark.parametrize("form", FORMS)
+@pytest.mark.parametrize("name,cfg,over,ld,strips,n_iter", _random_cases(), ids=[c[0] for c in _random_cases()])
+def test_random_shapes_against_oracle(name, cfg, over, ld, strips, n_iter, form):
+    strips = dict(strips, flags=_form_flags(form, over["head_dim"]))
+    wl = WORKLOADS["llama2-70b-gqa"].replace(key=name, cfg_id=cfg, n_iter=n_iter, std=0.02, **over)
+    wq, wk, v0, gq, gk = _cpu_case(wl, ld)
+    gpu = run_gpu(wl, gq, gk, v0, n_iter, want_u=True, ld=ld, **strips)
+    check_against_oracle(wl, _np(wq), _np(wk), v0, n_iter, gpu, want_u=True)

@@ -78,6 +78,26 @@ CASES = [
 ]
 
 
+def _random_cases(n=6, seed=2602):
+    """Seeded random shapes: 1..3 layers, ragged widths over padded rows,
+    1..600 tokens, d_h 16..128, MHA to 8 query heads per key head."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        d = int(rng.integers(16, 900))
+        ld = -(-d // 8) * 8 + 8 * int(rng.integers(0, 2))
+        n_kv = int(rng.integers(1, 4))
+        over = dict(n_layers=int(rng.integers(1, 4)), d_model=d, n_kv=n_kv, n_q=n_kv * int(rng.choice([1, 2, 3, 8])),
+                    head_dim=int(rng.choice([16, 32, 64, 128])))
+        seq = int(rng.integers(1, 601))
+        target = tuple(float(x) for x in rng.uniform(200.0, 700.0, over["n_layers"]))
+        out.append((f"rand{i}-d{d}-ld{ld}-q{over['n_q']}kv{n_kv}-dh{over['head_dim']}-seq{seq}", over, seq, ld, target))
+    return out
+
+
+CASES += _random_cases()
+
+
 @pytest.mark.parametrize("name,over,seq,ld,target", CASES, ids=[c[0] for c in CASES])
 def test_logits_against_oracle(name, over, seq, ld, target):
     wl = WORKLOADS["llama2-70b-gqa"].replace(key=name, std=0.02, **over)
@@ -105,7 +125,8 @@ def test_logits_against_oracle(name, over, seq, ld, target):
             nb, _ = check_head(codes[l, h], max_abs[l, h], n_over[l, h], xs[l], wq[l], wk[l], s32[l], h, wl.n_kv,
                                wl.head_dim)
             band += nb
-    assert n_over.sum() > 0
+    if max(target) > 450.0:
+        assert n_over.sum() > 0
     print(f"{name}: codes equal the oracle's outside the rounding bands ({band} entries inside one)")
     # statistics without codes are the same
     m2, o2, c2 = est.logits_fp8(x_dev, _pad(wq, ld), _pad(wk, ld), scale_dev, want_codes=False)

@@ -81,6 +81,26 @@ def _padded(w, ld, d):
     return p.cuda()[:, :, :d]
 
 
+def _random_cases(n=8, seed=933):
+    """Seeded random shapes: MHA and GQA, d_h 8..128, fp32 and bf16, ragged
+    widths over padded rows."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        dt = str(rng.choice(["f32", "bf16"]))
+        align = 4 if dt == "f32" else 8
+        d = int(rng.integers(8, 1200))
+        ld = -(-d // align) * align + align * int(rng.integers(0, 3))
+        n_kv = int(rng.integers(1, 4))
+        over = dict(n_layers=int(rng.integers(1, 4)), d_model=d, n_kv=n_kv, n_q=n_kv * int(rng.choice([1, 2, 3, 8])),
+                    head_dim=int(rng.choice([8, 16, 32, 64, 128])), dtype=dt, cfg_id=200 + i)
+        out.append((f"rand{i}-{dt}-d{d}-ld{ld}-q{over['n_q']}kv{n_kv}-dh{over['head_dim']}", over, ld))
+    return out
+
+
+CASES += _random_cases()
+
+
 @pytest.mark.parametrize("name,over,ld", CASES, ids=[c[0] for c in CASES])
 def test_layer_form_against_oracle(name, over, ld):
     wl = WORKLOADS["llama2-70b-gqa"].replace(key=name, n_iter=9, std=0.02, **over)

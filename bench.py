@@ -318,7 +318,7 @@ def bench_fp8(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1"}))
+        print(json.dumps({"error": "the estimator runs on one GPU (each GPU would hold its own shard of layers or heads); --gpus must be 1"}))
         sys.exit(2)
     if args.mode == "copy":
         copy_reference(args.copy_bytes)

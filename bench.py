@@ -51,6 +51,8 @@ def parse():
                         "layer-level estimator (one u, v per layer, spectral_step_layer); fp8: the E4M3 logit "
                         "consumer of the scale (spectral_logits_fp8) on --seq tokens per layer")
     p.add_argument("--seq", type=int, default=1024, help="tokens per layer of the fp8 form")
+    p.add_argument("--graph", action="store_true",
+                   help="chain/gram forms: capture one call into a HIP graph and time its replays")
     p.add_argument("--no-extras", action="store_true",
                    help="chain/gram forms: skip the context lines (one-iteration call, warm per-step call)")
     p.add_argument("--mode", choices=("bench", "copy"), default="bench",
@@ -359,12 +361,22 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    timed_step = step
+    if args.graph and not layer:
+        # the weight pointers are already on the device, so a call queues
+        # kernel launches only and can be captured
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        timed_step = graph.replay
+        for _ in range(args.warmup):
+            timed_step()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     e0.record()
     for _ in range(args.steps):
-        step()
+        timed_step()
     e1.record()
     torch.cuda.synchronize()
     wall_s = time.perf_counter() - t_wall
@@ -436,6 +448,7 @@ def main():
             "head_dim": wl.head_dim, "weights_dtype": wl.dtype, "n_iter": n_iter, "heads": H,
             "start": "cold (seeded unit vectors), state carried across steps",
             "form": args.form,
+            "launch": "HIP graph replay" if args.graph and not layer else "eager",
         },
         "effective_GBps": call_bytes / (ms * 1e-3) / 1e9,
         "effective_frac_of_peak": call_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,

@@ -137,8 +137,12 @@ SN_API int spectral_init(sn_ctx** ctx, const sn_shape* shape, const sn_params* p
  *              start vector, u = 0).
  * The call is queued asynchronously on the context's stream.  With tol > 0
  * it waits on the stream at iterations 2, 3, 4, 6, 9, ... to stop queueing
- * once every head has converged (not in the Gram form, which never waits).  Weights and vectors must not alias the
- * outputs.  Errors: SN_ENULL, SN_EINVAL, SN_EHIP. */
+ * once every head has converged (not in the Gram form, which never waits).
+ * The first call with a new set of weight pointers uploads them to a device
+ * table (hipMemcpyAsync from pinned memory); a call with the same pointers as
+ * the previous one, in either form with tol == 0, queues kernel launches
+ * only and can be captured into a HIP graph.  Weights and vectors must not
+ * alias the outputs.  Errors: SN_ENULL, SN_EINVAL, SN_EHIP. */
 SN_API int spectral_step(sn_ctx* ctx, const void* const* wq_layers, const void* const* wk_layers,
                          float* v, float* u, int32_t n_iter, float* sigma, float* scale,
                          int32_t* iters);
@@ -207,7 +211,9 @@ SN_API int spectral_logits_fp8(sn_ctx* ctx, const void* const* x_layers, int64_t
                                void* workspace, int64_t workspace_bytes, uint8_t* codes, float* max_abs,
                                int32_t* n_over);
 
-/* Redirects later calls to another hipStream_t. */
+/* Redirects later calls to another hipStream_t.  Unless that stream is being
+ * captured, it is first made to wait for the context's last upload of the
+ * weight-pointer table (queued on the previous stream). */
 SN_API int spectral_set_stream(sn_ctx* ctx, void* hip_stream);
 
 /* Frees the context and its workspace (waits for its queued work first). */

@@ -455,7 +455,15 @@ SN_API int spectral_init(sn_ctx** ctx, const sn_shape* shape, const sn_params* p
 
 SN_API int spectral_set_stream(sn_ctx* c, void* hip_stream) {
   if (!c) return fail(SN_ENULL, "ctx must not be NULL");
-  c->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+  // later launches read the device pointer table, whose last copy was queued
+  // on the previous stream: order the new stream after it (a stream being
+  // captured into a graph cannot wait on an outside event; its launches run
+  // at replay, after the copy)
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  SN_HIP(hipStreamIsCapturing(st, &cap));
+  if (cap == hipStreamCaptureStatusNone && st != c->stream) SN_HIP(hipStreamWaitEvent(st, c->tab_event, 0));
+  c->stream = st;
   return SN_OK;
 }
 

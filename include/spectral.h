@@ -137,7 +137,9 @@ SN_API int spectral_init(sn_ctx** ctx, const sn_shape* shape, const sn_params* p
  *              start vector, u = 0).
  * The call is queued asynchronously on the context's stream.  With tol > 0
  * it waits on the stream at iterations 2, 3, 4, 6, 9, ... to stop queueing
- * once every head has converged (not in the Gram form, which never waits).
+ * once every head has converged (not in the Gram form, which never waits);
+ * after a wait that finds at most half the heads running, the sweeps visit
+ * only the heads that still ran there.
  * The first call with a new set of weight pointers uploads them to a device
  * table (hipMemcpyAsync from pinned memory); a call with the same pointers as
  * the previous one, in either form with tol == 0, queues kernel launches
@@ -233,11 +235,12 @@ SN_API int spectral_workspace_bytes(const sn_shape* shape, const sn_params* para
  * iteration, 6 = final sweeps of the Gram form, 7 = row sweeps of the
  * layer-level form, 8 = its column sweeps, 9 = its reductions and
  * finalize, 10 = projections of the logit consumer, 11 = its logit
- * kernels), the summed device time in
+ * kernels, 12 = the running-head lists of tolerance mode), the summed
+ * device time in
  * milliseconds and the number of launches since the previous read, then
  * resets both.  ms and launches point to SN_PROFILE_KINDS host elements
  * each. */
-#define SN_PROFILE_KINDS 12
+#define SN_PROFILE_KINDS 13
 SN_API int spectral_profile(sn_ctx* ctx, int32_t enable);
 SN_API int spectral_profile_read(sn_ctx* ctx, double* ms, int64_t* launches);
 

@@ -44,6 +44,8 @@ struct Work {
   int32_t* n_alive;  // [2]             heads still running after a W_K sweep
   int32_t* iters;    // [H]             used when the caller passes no iters array
   float* fin;        // [H][2][DH]      Gram form: z and y of each head's last step
+  int32_t* zs;       // [H]             tolerance mode: strips of each head's last ||v'||^2 partials
+  int32_t* list;     // [H + U]         tolerance-mode tail: running query heads, then running W_K units
 };
 
 struct SweepArgs {
@@ -54,6 +56,7 @@ struct SweepArgs {
   int32_t s_out, tps, n_tiles, nch, n_items;
   int32_t k, n_iter, want_vec;
   float tol;
+  const int32_t* list;      // tail launches: the decoded unit of item index r is list[r] (-1: none)
   Work w;
   float* v;
   float* u;
@@ -64,6 +67,7 @@ struct SweepArgs {
 struct FinArgs {
   int32_t H, L, n_q, d, s_k;
   int32_t slot_fixed;  // workspace slot of the ||v'||^2 partials; -1: parity of the last step
+  const int32_t* zs;   // per-head strips of those partials, or nullptr: s_k for every head
   float coef;
   Work w;
   float* v;
@@ -139,6 +143,12 @@ struct LayerFinArgs {
 void launch_sweep(bool bf16, int head_dim, int ph, int gc, bool mfma, int n_items, hipStream_t st,
                   const SweepArgs& a);
 void launch_finalize(int blocks, hipStream_t st, const FinArgs& f);
+// Lists the heads still running after the W_K sweep of parity `slot` in
+// list_q[0 .. H) and the W_K units holding one of them in list_k[0 ..
+// n_units), both ascending and padded with -1, and clears the other parity's
+// flag of every stopped head.  One workgroup.
+void launch_tail_lists(const SweepArgs& a, int slot, int gc, int n_units, int32_t* list_q, int32_t* list_k,
+                       hipStream_t st);
 void launch_gram(bool bf16, int head_dim, int n_items, hipStream_t st, const GramArgs& g);
 void launch_gram_iterate(int head_dim, int heads, hipStream_t st, const IterArgs& a);
 void launch_layer_sweep(bool bf16, int head_dim, int mode, int n_items, hipStream_t st, const LayerArgs& a);

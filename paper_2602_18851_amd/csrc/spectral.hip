@@ -45,7 +45,7 @@ int fail(int code, const std::string& msg) {
 
 enum {
   KIND_INIT = 0, KIND_Q = 1, KIND_K = 2, KIND_FIN = 3, KIND_GRAM = 4, KIND_ITER = 5, KIND_EMIT = 6,
-  KIND_LROWS = 7, KIND_LCOLS = 8, KIND_LRED = 9, KIND_PROJ = 10, KIND_LOGITS = 11, KIND_N = 12
+  KIND_LROWS = 7, KIND_LCOLS = 8, KIND_LRED = 9, KIND_PROJ = 10, KIND_LOGITS = 11, KIND_TAIL = 12, KIND_N = 13
 };
 static_assert(KIND_N == SN_PROFILE_KINDS, "profile kinds");
 
@@ -56,12 +56,15 @@ struct Plan {
   int tile_cq, n_tiles_q;                    // W_Q sweep
   bool mfma_k;  // W_K sweeps on the matrix cores
   int s_q, tps_q, s_k, tps_k;
+  bool tail;    // tolerance mode of the default form: compacted launches once few heads run
+  int s_qmax, s_kmax;  // most strips any sweep of the plan writes (workspace sizing)
   bool gram;    // Gram form
   int units_g, s_g, tps_g, n_tiles_g, nb_g;
   bool layer;   // layer-level form
   int s_lq, tps_lq, s_lk, tps_lk;  // row / column strips of the layer-form sweeps over W_Q and W_K
   size_t off_zp, off_zn, off_yp, off_yn, off_sig, off_vn, off_alive, off_nalive, off_iters, off_fin, off_gp;
   size_t off_lz, off_ly, off_lcol, off_lu, off_lv, off_ln2, off_lstat;
+  size_t off_zs, off_list;
   size_t bytes;
 };
 
@@ -131,6 +134,16 @@ Plan make_plan(const sn_shape* s, const sn_params* p) {
   strips(pl.n_tiles, (int64_t)s->n_layers * s->n_kv_heads * pl.nch, p->k_strips,
          pl.mfma_k ? kKMfmaResident : kKTargetItems, pl.mfma_k, &pl.s_k, &pl.tps_k);
   pl.gram = (p->flags & SN_FLAG_GRAM) != 0;
+  // Tolerance mode: once at most half the heads still run, the sweeps launch
+  // the running heads (and the W_K units holding one) only, with strips
+  // chosen for that count; the buffers hold the most strips strips() gives.
+  pl.tail = p->tol > 0.f && !pl.gram;
+  pl.s_qmax = pl.s_q;
+  pl.s_kmax = pl.s_k;
+  if (pl.tail) {
+    pl.s_qmax = std::max(pl.s_q, std::max(1, pl.n_tiles_q / kMinTilesPerStrip));
+    pl.s_kmax = std::max(pl.s_k, std::max(1, pl.n_tiles / kMinTilesPerStrip));
+  }
   if (pl.gram) {
     const int rb = dh / 16;
     pl.nb_g = rb * (rb + 1) / 2;
@@ -145,15 +158,19 @@ Plan make_plan(const sn_shape* s, const sn_params* p) {
     return o;
   };
   const size_t H = pl.H;
-  pl.off_zp = take(2 * H * pl.s_k * dh * 4);
-  pl.off_zn = take(2 * H * pl.s_k * 4);
-  pl.off_yp = take(H * pl.s_q * dh * 4);
-  pl.off_yn = take(H * pl.s_q * 4);
+  pl.off_zp = take(2 * H * pl.s_kmax * dh * 4);
+  pl.off_zn = take(2 * H * pl.s_kmax * 4);
+  pl.off_yp = take(H * pl.s_qmax * dh * 4);
+  pl.off_yn = take(H * pl.s_qmax * 4);
   pl.off_sig = take(2 * H * 4);
   pl.off_vn = take(H * 4);
   pl.off_alive = take(2 * H * 4);
   pl.off_nalive = take(2 * 4);
   pl.off_iters = take(H * 4);
+  if (pl.tail) {
+    pl.off_zs = take(H * 4);
+    pl.off_list = take((H + (size_t)s->n_layers * s->n_kv_heads * pl.nch) * 4);
+  }
   if (pl.gram) {
     pl.off_fin = take(H * 2 * dh * 4);
     pl.off_gp = take((size_t)pl.units_g * pl.s_g * pl.nb_g * 256 * 4);
@@ -236,8 +253,17 @@ int timed(sn_ctx* c, int kind, F&& launch) {
   return SN_OK;
 }
 
-int run_sweep(sn_ctx* c, int ph, SweepArgs a) {
+// Compacted launch of the tolerance-mode tail: `count` entries of `list`
+// (query heads for a W_Q sweep, W_K units otherwise), `s` strips of `tps`
+// tiles each.
+struct TailLaunch {
+  const int32_t* list = nullptr;
+  int count = 0, s = 0, tps = 0;
+};
+
+int run_sweep(sn_ctx* c, int ph, SweepArgs a, const TailLaunch& tl = TailLaunch{}) {
   const Plan& pl = c->plan;
+  const int n_units = c->shape.n_layers * c->shape.n_kv_heads * pl.nch;
   if (ph == PH_Q || ph == PH_EQ) {
     a.mats = c->d_tab;
     a.s_out = pl.s_q;
@@ -249,7 +275,14 @@ int run_sweep(sn_ctx* c, int ph, SweepArgs a) {
     a.s_out = pl.s_k;
     a.tps = pl.tps_k;
     a.n_tiles = pl.n_tiles;
-    a.n_items = c->shape.n_layers * c->shape.n_kv_heads * pl.nch * pl.s_k;
+    a.n_items = n_units * pl.s_k;
+  }
+  if (tl.list) {
+    a.list = tl.list;
+    a.s_out = tl.s;
+    a.tps = tl.tps;
+    a.n_items = tl.count * tl.s;
+    if (a.n_items == 0) return SN_OK;
   }
   const int kind = ph == PH_INIT ? KIND_INIT : ph == PH_Q ? KIND_Q : ph == PH_K ? KIND_K : KIND_EMIT;
   return timed(c, kind, [&] {
@@ -328,24 +361,48 @@ int layer_reduce(sn_ctx* c, const float* col, int units, int mode, float* vec, f
 
 // The sweeps of the default form: first W_K sweep, then n_iter x (W_Q sweep,
 // W_K sweep).  In tolerance mode the host polls the count of running heads at
-// iterations 2, 3, 4, 6, 9, ... and stops queueing once it is zero.
+// iterations 2, 3, 4, 6, 9, ... and stops queueing once it is zero.  From a
+// poll that finds at most half the heads running, each sweep launches only
+// the heads (W_Q) and W_K units that held a running head at that poll, with
+// strips sized for their count; the lists are rebuilt at every later poll.
+// The strip count of a sweep's partials travels with them: a sweep reads its
+// producer's count (s_k or s_q of the args) and writes its own (s_out), and
+// the W_K sweep's slot stride uses its own count as well.
 int run_chain(sn_ctx* c, SweepArgs a, float* u) {
+  const Plan& pl = c->plan;
+  const int n_units = c->shape.n_layers * c->shape.n_kv_heads * pl.nch;
   int rc;
   a.k = 0;
   if ((rc = run_sweep(c, PH_INIT, a)) != SN_OK) return rc;
   int next_check = 2;
+  TailLaunch tq, tk;  // empty until the first compacting poll
   for (int k = 1; k <= a.n_iter; ++k) {
     a.k = k;
     a.want_vec = (u != nullptr) && (c->params.tol > 0.f || k == a.n_iter);
-    if ((rc = run_sweep(c, PH_Q, a)) != SN_OK) return rc;
+    if ((rc = run_sweep(c, PH_Q, a, tq)) != SN_OK) return rc;
     a.want_vec = 0;
-    if ((rc = run_sweep(c, PH_K, a)) != SN_OK) return rc;
+    a.s_q = tq.list ? tq.s : pl.s_q;  // the strips the W_Q sweep wrote
+    a.s_k = tk.list ? tk.s : pl.s_k;  // ... and those this W_K sweep writes
+    if ((rc = run_sweep(c, PH_K, a, tk)) != SN_OK) return rc;
     if (c->params.tol > 0.f && k == next_check && k < a.n_iter) {
       SN_HIP(hipMemcpyAsync(c->h_alive, c->w.n_alive + (k & 1), sizeof(int32_t), hipMemcpyDeviceToHost,
                             c->stream));
       SN_HIP(hipStreamSynchronize(c->stream));
-      if (c->h_alive[0] == 0) break;
+      const int n = c->h_alive[0];
+      if (n == 0) break;
       next_check = k < 4 ? k + 1 : k + k / 2;
+      if (pl.tail && n <= pl.H / 2) {
+        int32_t* list_q = c->w.list;
+        int32_t* list_k = c->w.list + pl.H;
+        rc = timed(c, KIND_TAIL, [&] { launch_tail_lists(a, k & 1, pl.gc, n_units, list_q, list_k, c->stream); });
+        if (rc != SN_OK) return rc;
+        tq.list = list_q;
+        tq.count = std::min(n, pl.H);
+        strips(pl.n_tiles_q, tq.count, 0, kQTargetItems, false, &tq.s, &tq.tps);
+        tk.list = list_k;
+        tk.count = std::min(n, n_units);
+        strips(pl.n_tiles, tk.count, 0, pl.mfma_k ? kKMfmaResident : kKTargetItems, pl.mfma_k, &tk.s, &tk.tps);
+      }
     }
   }
   return SN_OK;
@@ -449,6 +506,8 @@ SN_API int spectral_init(sn_ctx** ctx, const sn_shape* shape, const sn_params* p
   c->w.n_alive = reinterpret_cast<int32_t*>(c->ws + pl.off_nalive);
   c->w.iters = reinterpret_cast<int32_t*>(c->ws + pl.off_iters);
   c->w.fin = pl.gram ? reinterpret_cast<float*>(c->ws + pl.off_fin) : nullptr;
+  c->w.zs = pl.tail ? reinterpret_cast<int32_t*>(c->ws + pl.off_zs) : nullptr;
+  c->w.list = pl.tail ? reinterpret_cast<int32_t*>(c->ws + pl.off_list) : nullptr;
   *ctx = c;
   return SN_OK;
 }
@@ -548,6 +607,7 @@ SN_API int spectral_step(sn_ctx* c, const void* const* wq_layers, const void* co
   f.d = c->shape.d_model;
   f.s_k = pl.s_k;
   f.slot_fixed = pl.gram ? 0 : -1;
+  f.zs = pl.tail ? c->w.zs : nullptr;
   f.coef = scale_coef(c);
   f.w = c->w;
   f.v = v;

@@ -50,9 +50,14 @@ struct Item {
 template <int DH, int GC, int PH>
 __device__ __forceinline__ Item decode_item(const SweepArgs& a, int item) {
   Item it;
-  const bool valid_item = item < a.n_items;
+  bool valid_item = item < a.n_items;
   it.strip = valid_item ? item % a.s_out : 0;
-  const int rest = valid_item ? item / a.s_out : 0;
+  int rest = valid_item ? item / a.s_out : 0;
+  if (a.list && valid_item) {  // tail launch: only the listed heads / units
+    rest = uni(a.list[rest]);
+    valid_item = rest >= 0;
+    if (!valid_item) rest = 0;
+  }
   if (PH == PH_Q || PH == PH_EQ) {  // one query head per item
     it.layer = rest / a.n_q;
     it.row0 = (rest % a.n_q) * DH;
@@ -179,6 +184,7 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
           if (last[i]) {
             a.sigma[hh] = sigma;
             a.iters[hh] = a.k;
+            if (a.w.zs) a.w.zs[hh] = a.s_out;  // the strips of this sweep's ||v'||^2 partials
           }
         }
         a.w.alive[slot_cur * a.H + hh] = (act[i] && !last[i]) ? 1 : 0;
@@ -662,7 +668,8 @@ __global__ void __launch_bounds__(kThreads) finalize_kernel(FinArgs f) {
     if (it > 0) {
       float n2 = 0.f;
       const int slot = f.slot_fixed >= 0 ? f.slot_fixed : (it & 1);
-      for (int s = 0; s < f.s_k; ++s) n2 += f.w.zn[((size_t)slot * f.H + b) * f.s_k + s];
+      const int sk = f.zs ? f.zs[b] : f.s_k;
+      for (int s = 0; s < sk; ++s) n2 += f.w.zn[((size_t)slot * f.H + b) * sk + s];
       vs = 1.0f / sqrtf(n2);
       us = 1.0f / f.sigma[b];
       touch_v = true;
@@ -696,6 +703,72 @@ __global__ void __launch_bounds__(kThreads) finalize_kernel(FinArgs f) {
     }
     if (threadIdx.x == 0) f.scale[l] = nan_seen ? __builtin_nanf("") : f.coef * red[0];
   }
+}
+
+// Lists of the tolerance-mode tail, built by one workgroup after the W_K
+// sweep of parity `slot`: thread t owns a contiguous range of heads (then of
+// W_K units) and counts the running ones, and an exclusive scan of the counts
+// in LDS gives each thread its first place in the list, so both lists come
+// out in ascending order.  Entries past the last running one are -1 (up to
+// H, and up to n_units).  A head that stopped has its flag of the other
+// parity cleared too: it is not visited again, so no later sweep would.
+constexpr int kTailThreads = 1024;
+
+__device__ __forceinline__ int block_exclusive_scan(int x, int* buf, int* total) {
+  const int t = threadIdx.x;
+  buf[t] = x;
+  __syncthreads();
+  for (int off = 1; off < kTailThreads; off <<= 1) {
+    const int y = t >= off ? buf[t - off] : 0;
+    __syncthreads();
+    buf[t] += y;
+    __syncthreads();
+  }
+  const int incl = buf[t];
+  *total = buf[kTailThreads - 1];
+  __syncthreads();
+  return incl - x;
+}
+
+__global__ void __launch_bounds__(kTailThreads)
+tail_lists_kernel(SweepArgs a, int slot, int gc, int n_units, int32_t* list_q, int32_t* list_k) {
+  __shared__ int buf[kTailThreads];
+  const int t = threadIdx.x;
+  const int32_t* cur = a.w.alive + (size_t)slot * a.H;
+  int32_t* other = a.w.alive + (size_t)(slot ^ 1) * a.H;
+  int total = 0;
+
+  const int per_h = (a.H + kTailThreads - 1) / kTailThreads;
+  const int h0 = min(a.H, t * per_h), h1 = min(a.H, h0 + per_h);
+  int n = 0;
+  for (int hh = h0; hh < h1; ++hh) n += cur[hh] != 0 ? 1 : 0;
+  int pos = block_exclusive_scan(n, buf, &total);
+  for (int hh = h0; hh < h1; ++hh) {
+    if (cur[hh] != 0)
+      list_q[pos++] = hh;
+    else
+      other[hh] = 0;
+  }
+  for (int i = total + t; i < a.H; i += kTailThreads) list_q[i] = -1;
+
+  // unit u = (layer * n_kv + j) * nch + ch holds query heads
+  // layer * n_q + j * g + ch * gc + (0 .. min(gc, g - ch * gc) - 1)
+  auto running = [&](int un) {
+    const int grp = un / a.nch, ch = un % a.nch;
+    const int head0 = (grp / a.n_kv) * a.n_q + (grp % a.n_kv) * a.g + ch * gc;
+    const int nv = min(gc, a.g - ch * gc);
+    bool r = false;
+    for (int i = 0; i < nv; ++i) r = r || cur[head0 + i] != 0;
+    return r;
+  };
+  const int per_u = (n_units + kTailThreads - 1) / kTailThreads;
+  const int u0 = min(n_units, t * per_u), u1 = min(n_units, u0 + per_u);
+  int m = 0;
+  for (int un = u0; un < u1; ++un) m += running(un) ? 1 : 0;
+  pos = block_exclusive_scan(m, buf, &total);
+  for (int un = u0; un < u1; ++un)
+    if (running(un)) list_k[pos++] = un;
+  for (int i = total + t; i < n_units; i += kTailThreads) list_k[i] = -1;
 }
 
 template <typename T, int DH, int GC>
@@ -762,6 +835,11 @@ void launch_sweep(bool bf16, int head_dim, int ph, int gc, bool mfma, int n_item
 
 void launch_finalize(int blocks, hipStream_t st, const FinArgs& f) {
   finalize_kernel<<<dim3(blocks), kThreads, 0, st>>>(f);
+}
+
+void launch_tail_lists(const SweepArgs& a, int slot, int gc, int n_units, int32_t* list_q, int32_t* list_k,
+                       hipStream_t st) {
+  tail_lists_kernel<<<dim3(1), kTailThreads, 0, st>>>(a, slot, gc, n_units, list_q, list_k);
 }
 
 }  // namespace sn

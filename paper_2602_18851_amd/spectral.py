@@ -21,7 +21,8 @@ SN_FLAG_VALU_K_SWEEP = 1
 SN_FLAG_GRAM = 2
 SN_FLAG_LAYER = 4
 KIND_NAMES = ("k_sweep_first", "q_sweep", "k_sweep", "finalize", "gram_sweep", "gram_iterate", "gram_final_sweeps",
-              "layer_row_sweeps", "layer_col_sweeps", "layer_reduce", "logits_projection", "logits_fp8")
+              "layer_row_sweeps", "layer_col_sweeps", "layer_reduce", "logits_projection", "logits_fp8",
+              "tail_lists")
 SN_PROFILE_KINDS = len(KIND_NAMES)
 
 EXPORTED = (

@@ -24,7 +24,7 @@ if not torch.cuda.is_available():  # pragma: no cover - collected on CPU machines, 
     pytest.skip("needs a GPU", allow_module_level=True)
 
 from paper_2602_18851_amd import Spectral  # noqa: E402
-from paper_2602_18851_amd.spectral import SN_FLAG_GRAM  # noqa: E402
+from paper_2602_18851_amd.spectral import SN_FLAG_GRAM, SN_FLAG_VALU_K_SWEEP  # noqa: E402
 
 FORMS = {"chain": 0, "gram": SN_FLAG_GRAM}
 
@@ -148,6 +148,55 @@ def test_tolerance_mode_on_planted_spectra(form):
             WQ, WK = head_slices(_np(wq)[l], _np(wk)[l], h, wl.n_kv, wl.head_dim)
             _check_tolerance_stop(gpu["iters"][l, h], gpu["sigma"][l, h], WQ, WK, v0[l, h].double().numpy(),
                                   1e-4, 2000)
+
+
+TAIL_CASES = [
+    # (id, shape overrides, flags): planted spectra, cold start, so the heads
+    # stop anywhere from ~10 to ~100 steps and the later sweeps run compacted
+    ("gqa8-bf16-dh64-mfma", dict(n_layers=3, d_model=1024, n_q=16, n_kv=2, head_dim=64), 0),
+    ("gqa8-bf16-dh64-valu", dict(n_layers=3, d_model=1024, n_q=16, n_kv=2, head_dim=64), SN_FLAG_VALU_K_SWEEP),
+    ("gqa12-bf16-dh128", dict(n_layers=2, d_model=512, n_q=24, n_kv=2, head_dim=128), 0),
+    ("mha-f32-dh32", dict(n_layers=2, d_model=256, n_q=8, n_kv=8, head_dim=32, dtype="f32"), 0),
+]
+
+
+@pytest.mark.parametrize("name,over,flags", TAIL_CASES, ids=[c[0] for c in TAIL_CASES])
+def test_tolerance_tail_every_head(name, over, flags):
+    """Tolerance mode once most heads have stopped: the sweeps then launch
+    only the running heads (and the W_K units holding one), with other strip
+    counts.  Every head is held to the oracle: sigma of its stopping step,
+    the stopping rule, and v, u of that step."""
+    wl = WORKLOADS["llama2-70b-perstep"].replace(key=name, **over)
+    wq, wk, v0, gq, gk = _cpu_case(wl)
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=1e-4,
+                   flags=flags)
+    est.profile(True)
+    v = v0.cuda().contiguous()
+    u = torch.empty_like(v)
+    sigma, scale, iters = est.step(gq, gk, v, 400, u=u)
+    torch.cuda.synchronize()
+    prof = est.profile_read()
+    est.close()
+    it = iters.cpu().numpy()
+    sigma, scale, v, u = sigma.cpu().numpy(), scale.cpu().numpy(), v.cpu().double().numpy(), u.cpu().double().numpy()
+    assert prof["tail_lists"][1] >= 1, prof["tail_lists"]   # the compacted launches ran
+    assert it.min() >= 2 and it.max() < 400
+    worst = 0.0
+    for l in range(wl.n_layers):
+        for h in range(wl.n_q):
+            WQ, WK = head_slices(_np(wq)[l], _np(wk)[l], h, wl.n_kv, wl.head_dim)
+            vs = v0[l, h].double().numpy()
+            _, e = _check_tolerance_stop(it[l, h], sigma[l, h], WQ, WK, vs, 1e-4, 400)
+            r = power_iteration(WQ, WK, vs, int(it[l, h]))
+            dv = np.linalg.norm(v[l, h] - r.v)
+            du = np.linalg.norm(u[l, h] - r.u)
+            assert dv <= RTOL and du <= RTOL, (l, h, it[l, h], dv, du)
+            worst = max(worst, e, dv, du)
+    ref_scale = np.array([layer_scale(sigma[l].astype(np.float64).max(), wl.alpha, wl.d_model, wl.head_dim)
+                          for l in range(wl.n_layers)])
+    assert _rel(scale, ref_scale).max() <= RTOL
+    print(f"{name}: iters {it.min()}..{it.max()} (median {np.median(it)}), "
+          f"{prof['tail_lists'][1]} list builds, worst {worst:.3e}")
 
 
 @pytest.mark.parametrize("form", FORMS)

@@ -312,9 +312,37 @@ def bench_fp8(args):
             "logits_kernel_TFLOPs": logit_flops / (l_ms / max(l_n - 1, 1) * 1e-3) / 1e12,
         },
     }
+    if not args.no_extras:
+        out["context"] = {"library_gemm": library_projection(x, wq, wk, proj_flops)}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline_fp8(wl, args.cpu_seconds, seq)
     print(json.dumps(out), flush=True)
+
+
+def library_projection(x, wq, wk, flops: float) -> dict:
+    """The projections of the consumer as plain library GEMMs (torch linear,
+    one per layer and matrix, bf16 in and out, fp32 accumulation), timed the
+    same way: a yardstick for the hand-written projection kernel."""
+    import torch
+    import torch.nn.functional as F
+
+    def run():
+        for l in range(x.shape[0]):
+            F.linear(x[l], wq[l])
+            F.linear(x[l], wk[l])
+
+    run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 5
+    e0.record()
+    for _ in range(reps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return {"what": "torch.nn.functional.linear per layer for Q and K (hipBLASLt), same shapes, bf16 output",
+            "ms": ms, "TFLOPs": flops / (ms * 1e-3) / 1e12}
 
 
 def main():

@@ -17,6 +17,8 @@ constexpr int kCPL = 8;               // 16-byte column chunks per wave row (lan
 constexpr int kMaxGC = 8;             // query heads per W_K work item
 constexpr int kQTargetItems = 10240;  // wave work items aimed for in a W_Q sweep
 constexpr int kMinTilesPerStrip = 4;  // automatic strips: at least this many tiles per wave
+constexpr int kTailMinTiles = 4;      // ... in the compacted launches of the tolerance-mode tail
+constexpr int kSetupUnroll = 4;       // producer partials summed per round in a sweep's set-up
 constexpr int kKTargetItems = 4096;   // ... and in a W_K sweep (register-heavier waves)
 constexpr int kKMfmaResident = 2048;  // waves of the matrix-core W_K sweep resident at once (256 CUs x 8)
 constexpr int kStreamPolicy = 2;       // cache policy of the weight loads: non-temporal (read once per sweep)

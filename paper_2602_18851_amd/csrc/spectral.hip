@@ -103,10 +103,11 @@ int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 // target / units (rounded up, or down when all waves should be resident at
 // once), with at least kMinTilesPerStrip tiles per strip so that a wave's
 // stream outweighs its prologue (which sums one partial per producer strip).
-void strips(int n_tiles, int64_t units, int requested, int target, bool round_down, int* s_out, int* tps_out) {
+void strips(int n_tiles, int64_t units, int requested, int target, bool round_down, int* s_out, int* tps_out,
+            int min_tiles = kMinTilesPerStrip) {
   const int64_t u = std::max<int64_t>(units, 1);
   int s = requested > 0 ? requested : round_down ? (int)std::max<int64_t>(1, target / u) : ceil_div(target, u);
-  if (requested <= 0) s = std::min(s, std::max(1, n_tiles / kMinTilesPerStrip));
+  if (requested <= 0) s = std::min(s, std::max(1, n_tiles / min_tiles));
   s = std::max(1, std::min(s, n_tiles));
   const int tps = ceil_div(n_tiles, s);
   *tps_out = tps;
@@ -141,8 +142,8 @@ Plan make_plan(const sn_shape* s, const sn_params* p) {
   pl.s_qmax = pl.s_q;
   pl.s_kmax = pl.s_k;
   if (pl.tail) {
-    pl.s_qmax = std::max(pl.s_q, std::max(1, pl.n_tiles_q / kMinTilesPerStrip));
-    pl.s_kmax = std::max(pl.s_k, std::max(1, pl.n_tiles / kMinTilesPerStrip));
+    pl.s_qmax = std::max(pl.s_q, std::max(1, pl.n_tiles_q / kTailMinTiles));
+    pl.s_kmax = std::max(pl.s_k, std::max(1, pl.n_tiles / kTailMinTiles));
   }
   if (pl.gram) {
     const int rb = dh / 16;
@@ -398,10 +399,11 @@ int run_chain(sn_ctx* c, SweepArgs a, float* u) {
         if (rc != SN_OK) return rc;
         tq.list = list_q;
         tq.count = std::min(n, pl.H);
-        strips(pl.n_tiles_q, tq.count, 0, kQTargetItems, false, &tq.s, &tq.tps);
+        strips(pl.n_tiles_q, tq.count, 0, kQTargetItems, false, &tq.s, &tq.tps, kTailMinTiles);
         tk.list = list_k;
         tk.count = std::min(n, n_units);
-        strips(pl.n_tiles, tk.count, 0, pl.mfma_k ? kKMfmaResident : kKTargetItems, pl.mfma_k, &tk.s, &tk.tps);
+        strips(pl.n_tiles, tk.count, 0, pl.mfma_k ? kKMfmaResident : kKTargetItems, pl.mfma_k, &tk.s, &tk.tps,
+               kTailMinTiles);
       }
     }
   }

@@ -204,7 +204,7 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
   for (int i = 0; i < GC; ++i)
 #pragma unroll
     for (int rr = 0; rr < NR; ++rr) xv[i][rr] = 0.f;
-#pragma unroll 4
+#pragma unroll kSetupUnroll
   for (int t = 0; t < s_in; ++t) {
 #pragma unroll
     for (int i = 0; i < GC; ++i) {

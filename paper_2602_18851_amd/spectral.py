@@ -275,7 +275,20 @@ class Spectral:
     def _layer_ptrs(self, w, rows: int) -> list[int]:
         import torch
 
-        layers = list(w.unbind(0)) if isinstance(w, torch.Tensor) and w.dim() == 3 else list(w)
+        if isinstance(w, torch.Tensor) and w.dim() == 3:
+            # one stacked tensor: checked once, layer l starts l * stride(0) elements in
+            L = self.shape.n_layers
+            if w.shape[0] != L:
+                raise ValueError(f"expected {L} layers, got {w.shape[0]}")
+            if not w.is_cuda or w.dtype != self.torch_dtype:
+                raise ValueError(f"weights must be {self.torch_dtype} CUDA tensors")
+            if w.shape[1] != rows or w.shape[2] < self.shape.d_model:
+                raise ValueError(f"layer weight must be [{rows}, >= {self.shape.d_model}], got {tuple(w.shape[1:])}")
+            if w.stride(2) != 1 or w.stride(1) != self.ld:
+                raise ValueError(f"layer weight must be row-major with row stride {self.ld}")
+            base, step = w.data_ptr(), w.stride(0) * w.element_size()
+            return [base + l * step for l in range(L)]
+        layers = list(w)
         if len(layers) != self.shape.n_layers:
             raise ValueError(f"expected {self.shape.n_layers} layers, got {len(layers)}")
         ptrs = []

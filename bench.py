@@ -420,9 +420,9 @@ def main():
     q_bytes, k_bytes = wl.weight_bytes()
     dom_launch_bytes = None
     if layer:
-        # per step: row sweeps over W_K and W_Q; column sweeps over W_Q and W_K that
-        # write one d-vector per query / key head; the per-layer sums read them back
-        col_buf = (H + wl.n_layers * wl.n_kv) * wl.d_model * 4
+        # per step: row sweeps over W_K and W_Q; column sweeps over W_Q and W_K,
+        # which read one d_h-vector per query / key head and write u' and v'
+        col_buf = (H + wl.n_layers * wl.n_kv) * wl.head_dim * 4 + 2 * wl.n_layers * wl.d_model * 4
         r_ms, r_n = prof["layer_row_sweeps"]
         c_ms, c_n = prof["layer_col_sweeps"]
         if r_ms >= c_ms:
@@ -433,7 +433,7 @@ def main():
                 n_iter * (q_bytes + k_bytes + col_buf)
         dom_launch_bytes = dom_alg  # all launches of the kind together
         dom_flops = None
-        call_bytes = n_iter * (2 * (q_bytes + k_bytes) + 2 * col_buf) + 12 * wl.d_model * wl.n_layers
+        call_bytes = n_iter * (2 * (q_bytes + k_bytes) + col_buf) + 12 * wl.d_model * wl.n_layers
         H = wl.n_layers  # one estimate per layer
     elif gram:
         # Gram sweep: every weight read once, the upper-triangle 16 x 16 Gram

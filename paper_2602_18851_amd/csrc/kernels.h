@@ -100,27 +100,46 @@ struct IterArgs {
 struct LayerArgs {
   const void* const* mats;  // device table of this matrix's per-layer pointers
   int64_t ld;
-  int32_t d, units, n_items, s_out, tps, n_tiles;
+  int32_t d, n_tiles, n_items;
   const int32_t* lstat;     // [L]
-  // rows sweep: x = xvec[layer] / sqrt(xn2[layer]) -> rowpart [L*units][s_out][DH]
+  // rows sweep, item = (layer * units + unit) * s_out + strip:
+  // x = xvec[layer] / sqrt(xn2[layer]) -> rowpart [L*units][s_out][DH]
+  int32_t units, s_out, tps;
   const float* xvec;
   const float* xn2;
   float* rowpart;
-  // cols sweep: y = sum over y_cnt source units starting at (ul / y_div) * y_cnt
-  // of the source rows sweep's partials (y_units per layer, y_strips strips)
-  const float* ypart;
-  int32_t y_units, y_strips, y_div, y_cnt;
-  float* colout;            // [L*units][d]
+  // cols sweep, item = (layer * n_rsplit + rs) * n_tiles + tile: one column
+  // tile of the layer over row blocks rs * rb_per .. (of nrb), each block b
+  // weighted by vin[layer][b] -> colout [L * n_rsplit][cstride]
+  int32_t nrb, n_rsplit, rb_per;
+  const float* vin;         // [L][nrb][DH]
+  float* colout;            // columns 0 .. d - 1 of each row are written
+  int32_t cstride;          // multiple of 64 and >= d
+};
+
+// Inputs of a column sweep, one d_h-vector per row block of the swept matrix:
+// vin[l][b] = sum over the cnt source units starting at (b / div) * cnt of
+// their strip partials (src_units units per layer, strips strips each), in
+// unit then strip order.
+struct LayerVinArgs {
+  const float* part;
+  int32_t src_units, strips, div, cnt, nrb, dh;
+  const int32_t* lstat;
+  float* vin;
 };
 
 // Per layer: vec[c] = sum over the layer's units of col[unit][c] (fixed order)
 // and n2 = ||vec||^2; mode 0 copies the caller's start vector instead and
-// (re)initialises the layer status; mode 1 marks M v = 0.
+// (re)initialises the layer status; mode 1 marks M v = 0.  Two launches: the
+// column sums over nb blocks of kRedThreads columns per layer, each leaving
+// its part of n2 in n2part[layer][block], then one block per layer that adds
+// the parts in block order.
 struct LayerReduceArgs {
-  const float* col;
-  int32_t units, d, mode;
+  const float* col;         // [L*units][cstride]
+  int32_t units, d, cstride, mode, nb;
   float* vec;
   float* n2;
+  float* n2part;    // [L][nb]
   float* n2_start;  // mode 0: ||v||^2 of the start vector
   int32_t* lstat;
 };
@@ -154,6 +173,7 @@ void launch_tail_lists(const SweepArgs& a, int slot, int gc, int n_units, int32_
 void launch_gram(bool bf16, int head_dim, int n_items, hipStream_t st, const GramArgs& g);
 void launch_gram_iterate(int head_dim, int heads, hipStream_t st, const IterArgs& a);
 void launch_layer_sweep(bool bf16, int head_dim, int mode, int n_items, hipStream_t st, const LayerArgs& a);
+void launch_layer_vin(int layers, hipStream_t st, const LayerVinArgs& v);
 void launch_layer_reduce(int layers, hipStream_t st, const LayerReduceArgs& r);
 void launch_layer_finalize(int layers, hipStream_t st, const LayerFinArgs& f);
 

@@ -61,9 +61,10 @@ struct Plan {
   bool gram;    // Gram form
   int units_g, s_g, tps_g, n_tiles_g, nb_g;
   bool layer;   // layer-level form
-  int s_lq, tps_lq, s_lk, tps_lk;  // row / column strips of the layer-form sweeps over W_Q and W_K
+  int s_lq, tps_lq, s_lk, tps_lk;  // strips of the layer-form row sweeps over W_Q and W_K
+  int rs_q, rbp_q, rs_k, rbp_k;    // row splits (and row blocks per split) of its column sweeps
   size_t off_zp, off_zn, off_yp, off_yn, off_sig, off_vn, off_alive, off_nalive, off_iters, off_fin, off_gp;
-  size_t off_lz, off_ly, off_lcol, off_lu, off_lv, off_ln2, off_lstat;
+  size_t off_lz, off_ly, off_lvin, off_lcol, off_lu, off_lv, off_ln2, off_ln2p, off_lstat;
   size_t off_zs, off_list;
   size_t bytes;
 };
@@ -98,6 +99,9 @@ int validate(const sn_shape* s, const sn_params* p) {
 }
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+// Row stride of the layer form's per-unit column sums: whole 64-column tiles.
+int col_stride(int d) { return ceil_div(d, 64) * 64; }
 
 // Column strips per unit (head or KV head): the request if given, else about
 // target / units (rounded up, or down when all waves should be resident at
@@ -183,10 +187,22 @@ Plan make_plan(const sn_shape* s, const sn_params* p) {
     strips(pl.n_tiles_q, (int64_t)Hk, 0, kQTargetItems, false, &pl.s_lk, &pl.tps_lk);
     pl.off_lz = take(Hk * pl.s_lk * dh * 4);
     pl.off_ly = take(H * pl.s_lq * dh * 4);
-    pl.off_lcol = take(H * d * 4);
+    // column sweeps: one wave per column tile and row split; rows are split
+    // only as far as needed for about kQTargetItems waves
+    auto rsplit = [&](int nrb, int* n_split, int* per) {
+      const int64_t base = (int64_t)L * pl.n_tiles_q;
+      const int want = (int)std::min<int64_t>(nrb, std::max<int64_t>(1, (kQTargetItems + base - 1) / base));
+      *per = ceil_div(nrb, want);
+      *n_split = ceil_div(nrb, *per);
+    };
+    rsplit(s->n_q_heads, &pl.rs_q, &pl.rbp_q);
+    rsplit(s->n_kv_heads, &pl.rs_k, &pl.rbp_k);
+    pl.off_lvin = take(H * dh * 4);
+    pl.off_lcol = take(L * (size_t)std::max(pl.rs_q, pl.rs_k) * col_stride(s->d_model) * 4);
     pl.off_lu = take(L * d * 4);
     pl.off_lv = take(L * d * 4);
     pl.off_ln2 = take(3 * L * 4);
+    pl.off_ln2p = take(L * (size_t)ceil_div(d, kRedThreads) * 4);
     pl.off_lstat = take(L * 4);
   }
   pl.bytes = off;
@@ -334,26 +350,53 @@ int layer_sweep(sn_ctx* c, bool q, int mode, LayerArgs a) {
   a.mats = c->d_tab + (q ? 0 : L);
   a.ld = c->shape.ld;
   a.d = c->shape.d_model;
-  a.units = q ? c->shape.n_q_heads : c->shape.n_kv_heads;
-  a.s_out = q ? pl.s_lq : pl.s_lk;
-  a.tps = q ? pl.tps_lq : pl.tps_lk;
   a.n_tiles = pl.n_tiles_q;
-  a.n_items = L * a.units * a.s_out;
   a.lstat = reinterpret_cast<const int32_t*>(c->ws + pl.off_lstat);
+  if (mode == LM_ROWS) {
+    a.units = q ? c->shape.n_q_heads : c->shape.n_kv_heads;
+    a.s_out = q ? pl.s_lq : pl.s_lk;
+    a.tps = q ? pl.tps_lq : pl.tps_lk;
+    a.n_items = L * a.units * a.s_out;
+  } else {
+    a.nrb = q ? c->shape.n_q_heads : c->shape.n_kv_heads;
+    a.n_rsplit = q ? pl.rs_q : pl.rs_k;
+    a.rb_per = q ? pl.rbp_q : pl.rbp_k;
+    a.cstride = col_stride(c->shape.d_model);
+    a.n_items = L * a.n_rsplit * a.n_tiles;
+  }
   return timed(c, mode == LM_ROWS ? KIND_LROWS : KIND_LCOLS, [&] {
     launch_layer_sweep(c->shape.dtype == SN_BF16, c->shape.head_dim, mode, a.n_items, c->stream, a);
   });
 }
 
-int layer_reduce(sn_ctx* c, const float* col, int units, int mode, float* vec, float* n2) {
+// vin of a column sweep from the previous row sweep's partials.
+int layer_vin(sn_ctx* c, const float* part, int src_units, int strips, int div, int cnt, int nrb) {
+  const Plan& pl = c->plan;
+  LayerVinArgs v{};
+  v.part = part;
+  v.src_units = src_units;
+  v.strips = strips;
+  v.div = div;
+  v.cnt = cnt;
+  v.nrb = nrb;
+  v.dh = c->shape.head_dim;
+  v.lstat = reinterpret_cast<const int32_t*>(c->ws + pl.off_lstat);
+  v.vin = reinterpret_cast<float*>(c->ws + pl.off_lvin);
+  return timed(c, KIND_LRED, [&] { launch_layer_vin(c->shape.n_layers, c->stream, v); });
+}
+
+int layer_reduce(sn_ctx* c, const float* col, int units, int cstride, int mode, float* vec, float* n2) {
   const Plan& pl = c->plan;
   LayerReduceArgs r{};
   r.col = col;
   r.units = units;
   r.d = c->shape.d_model;
+  r.cstride = cstride;
   r.mode = mode;
   r.vec = vec;
   r.n2 = n2;
+  r.nb = ceil_div(c->shape.d_model, kRedThreads);
+  r.n2part = reinterpret_cast<float*>(c->ws + pl.off_ln2p);
   r.n2_start = reinterpret_cast<float*>(c->ws + pl.off_ln2) + 2 * c->shape.n_layers;
   r.lstat = reinterpret_cast<int32_t*>(c->ws + pl.off_lstat);
   return timed(c, KIND_LRED,
@@ -634,41 +677,38 @@ SN_API int spectral_step_layer(sn_ctx* c, const void* const* wq_layers, const vo
   float* lz = reinterpret_cast<float*>(c->ws + pl.off_lz);
   float* ly = reinterpret_cast<float*>(c->ws + pl.off_ly);
   float* lcol = reinterpret_cast<float*>(c->ws + pl.off_lcol);
+  float* lvin = reinterpret_cast<float*>(c->ws + pl.off_lvin);
   float* lu = reinterpret_cast<float*>(c->ws + pl.off_lu);
   float* lv = reinterpret_cast<float*>(c->ws + pl.off_lv);
   float* n2_u = reinterpret_cast<float*>(c->ws + pl.off_ln2);
   float* n2_v = n2_u + L;
   // start vectors: copy, squared norms, layer status
-  if ((rc = layer_reduce(c, v, 1, 0, lv, n2_v)) != SN_OK) return rc;
+  if ((rc = layer_reduce(c, v, 1, c->shape.d_model, 0, lv, n2_v)) != SN_OK) return rc;
   for (int k = 1; k <= n_iter; ++k) {
     LayerArgs a{};
     a.xvec = lv;  // z_j = K_j v
     a.xn2 = n2_v;
     a.rowpart = lz;
     if ((rc = layer_sweep(c, false, LM_ROWS, a)) != SN_OK) return rc;
-    a = LayerArgs{};  // c_h = Q_h^T z_{j(h)}: RepeatBlocks
-    a.ypart = lz;
-    a.y_units = c->shape.n_kv_heads;
-    a.y_strips = pl.s_lk;
-    a.y_div = pl.g;
-    a.y_cnt = 1;
+    // u' = sum_h Q_h^T z_j(h): RepeatBlocks, then one column sweep over W_Q
+    if ((rc = layer_vin(c, lz, c->shape.n_kv_heads, pl.s_lk, pl.g, 1, c->shape.n_q_heads)) != SN_OK) return rc;
+    a = LayerArgs{};
+    a.vin = lvin;
     a.colout = lcol;
     if ((rc = layer_sweep(c, true, LM_COLS, a)) != SN_OK) return rc;
-    if ((rc = layer_reduce(c, lcol, c->shape.n_q_heads, 1, lu, n2_u)) != SN_OK) return rc;
+    if ((rc = layer_reduce(c, lcol, pl.rs_q, col_stride(c->shape.d_model), 1, lu, n2_u)) != SN_OK) return rc;
     a = LayerArgs{};  // y_h = Q_h u
     a.xvec = lu;
     a.xn2 = n2_u;
     a.rowpart = ly;
     if ((rc = layer_sweep(c, true, LM_ROWS, a)) != SN_OK) return rc;
-    a = LayerArgs{};  // c_j = K_j^T sum_{h in j} y_h: SumGroups
-    a.ypart = ly;
-    a.y_units = c->shape.n_q_heads;
-    a.y_strips = pl.s_lq;
-    a.y_div = 1;
-    a.y_cnt = pl.g;
+    // v' = sum_j K_j^T sum_{h in j} y_h: SumGroups, then one column sweep over W_K
+    if ((rc = layer_vin(c, ly, c->shape.n_q_heads, pl.s_lq, 1, pl.g, c->shape.n_kv_heads)) != SN_OK) return rc;
+    a = LayerArgs{};
+    a.vin = lvin;
     a.colout = lcol;
     if ((rc = layer_sweep(c, false, LM_COLS, a)) != SN_OK) return rc;
-    if ((rc = layer_reduce(c, lcol, c->shape.n_kv_heads, 2, lv, n2_v)) != SN_OK) return rc;
+    if ((rc = layer_reduce(c, lcol, pl.rs_k, col_stride(c->shape.d_model), 2, lv, n2_v)) != SN_OK) return rc;
   }
   LayerFinArgs f{};
   f.d = c->shape.d_model;

@@ -70,6 +70,9 @@ CASES = [
     ("gqa3-bf16-ragged", dict(n_layers=1, d_model=1001, n_q=6, n_kv=2, head_dim=32, dtype="bf16"), 1008),
     ("mqa-bf16-dh8", dict(n_layers=2, d_model=64, n_q=8, n_kv=1, head_dim=8, dtype="bf16"), 0),
     ("gqa4-f32-ragged-dh16", dict(n_layers=3, d_model=517, n_q=8, n_kv=2, head_dim=16, dtype="f32"), 520),
+    # 2 layers x 64 column tiles: the W_Q column sweep splits its 99 row blocks
+    # into 50 runs of two (the last run one block), each wave summing its run
+    ("gqa33-bf16-row-runs", dict(n_layers=2, d_model=4096, n_q=99, n_kv=3, head_dim=8, dtype="bf16"), 0),
 ]
 
 

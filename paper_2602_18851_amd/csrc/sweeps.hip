@@ -17,6 +17,11 @@
 //     reads every K_j element once and applies it to all query heads of the
 //     chunk from registers (the implicit-GQA form of Sec. 4.2 without key
 //     expansion): v'[c] = sum_r K[r,c] y_h[r], ||v'||^2, z_h[r] partials.
+//     With bf16 weights and 3..8 query heads per KV head, ksweep_mfma_kernel
+//     does this on the matrix cores from a tile staged once in LDS.
+// In tolerance mode, once few heads still run, the sweeps are launched over
+// lists of the running query heads and of the W_K units that hold one
+// (tail_lists_kernel), item r decoding to list entry r instead of r itself.
 // Partials (one d_h vector and one squared norm per strip) go to a small
 // workspace and are summed, in a fixed order, by the consumer of the next
 // sweep, which also normalises (y /= sigma, z /= ||v'||).  Every reduction

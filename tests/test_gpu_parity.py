@@ -160,6 +160,29 @@ TAIL_CASES = [
 ]
 
 
+def _random_tail_cases(n=8, seed=7106):
+    """Seeded random planted shapes for the tail: 1 to 12 query heads per key
+    head (partial W_K chunks at 12), d_h 16..128, fp32 and bf16, both W_K
+    sweeps."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        dt = str(rng.choice(["f32", "bf16"]))
+        dh = int(rng.choice([16, 32, 64, 128]))
+        d = int(rng.choice([256, 512, 1024]))
+        n_kv = int(rng.integers(1, 4))
+        g = int(rng.choice([1, 2, 3, 5, 8, 12]))
+        flags = int(rng.choice([0, SN_FLAG_VALU_K_SWEEP]))
+        over = dict(n_layers=int(rng.integers(1, 4)), d_model=d, n_q=n_kv * g, n_kv=n_kv, head_dim=dh, dtype=dt,
+                    cfg_id=300 + i)
+        out.append((f"rand{i}-{dt}-d{d}-q{n_kv * g}kv{n_kv}-dh{dh}-f{flags}", over, flags))
+    return out
+
+
+TAIL_CASES += _random_tail_cases()
+POLLS = (2, 3, 4, 6, 9, 13, 19, 28, 42, 63, 94, 141, 211, 316)
+
+
 @pytest.mark.parametrize("name,over,flags", TAIL_CASES, ids=[c[0] for c in TAIL_CASES])
 def test_tolerance_tail_every_head(name, over, flags):
     """Tolerance mode once most heads have stopped: the sweeps then launch
@@ -179,7 +202,10 @@ def test_tolerance_tail_every_head(name, over, flags):
     est.close()
     it = iters.cpu().numpy()
     sigma, scale, v, u = sigma.cpu().numpy(), scale.cpu().numpy(), v.cpu().double().numpy(), u.cpu().double().numpy()
-    assert prof["tail_lists"][1] >= 1, prof["tail_lists"]   # the compacted launches ran
+    # the compacted launches ran if some poll before the last step saw at most half the heads running
+    H = it.size
+    expect = any(0 < int((it > k).sum()) <= H // 2 for k in POLLS if k < it.max())
+    assert (prof["tail_lists"][1] >= 1) == expect, (prof["tail_lists"], expect)
     assert it.min() >= 2 and it.max() < 400
     worst = 0.0
     for l in range(wl.n_layers):

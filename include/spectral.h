@@ -76,7 +76,10 @@ typedef struct {
   float r_max;         /* largest finite FP8 magnitude, 448 for OCP E4M3          */
   float tol;           /* 0: run exactly n_iter iterations.  > 0: stop a head
                           after step k >= 2 once |sigma_k - sigma_{k-1}| <=
-                          tol * sigma_k, with n_iter as the cap.                  */
+                          tol * sigma_k, with n_iter as the cap.  The workspace
+                          then also holds the partials of the compacted sweeps
+                          (up to one strip per 4 column tiles per head; 254 MB
+                          at 80 x 64 heads of d_h 128, d 8192).                   */
   int32_t q_strips;    /* column strips per head in the W_Q sweep; 0 = automatic  */
   int32_t k_strips;    /* column strips per KV head in the W_K sweep; 0 = auto    */
   int32_t flags;       /* SN_FLAG_* bits; 0 for the defaults                      */
@@ -101,9 +104,11 @@ typedef struct {
  * and column strip (spectral_workspace_bytes gives the total). */
 #define SN_FLAG_GRAM 2
 
-/* Reserve the workspace of the layer-level form (spectral_step_layer):
- * about (n_layers * n_q * d_model + 2 * n_layers * d_model) * 4 bytes more.
- * spectral_step itself is unaffected. */
+/* Reserve the workspace of the layer-level form (spectral_step_layer): the
+ * row-sweep partials, one d_h-vector per query head, the column sums (one row
+ * of d_model rounded up to 64 per layer and row split, up to n_q splits on
+ * small shapes) and per-layer vectors; spectral_workspace_bytes gives the
+ * total.  spectral_step itself is unaffected. */
 #define SN_FLAG_LAYER 4
 
 

@@ -130,6 +130,33 @@ def cpu_baseline(wl, budget_s: float, n_iter: int):
     }
 
 
+def cpu_explicit_m(wl, budget_s: float, n_iter: int):
+    """The route the method avoids, timed beside the baseline: the oracle's
+    cross-check that forms M = Q_h^T K_j (d x d, float64) per head and runs
+    dense power iteration on it, over at least one head and as many more of
+    layer 0 as fit in the budget."""
+    import numpy as np
+
+    from oracle.explicit import dense_power_iteration, interaction_matrix
+    from oracle.power_iteration import head_slices
+    from workloads import layer_weights, start_vectors
+
+    v0 = start_vectors(wl.replace(n_layers=1), "cpu")[0].double().numpy()
+    wq, wk = layer_weights(wl, 0, "cpu")
+    wq, wk = wq.float().numpy(), wk.float().numpy()
+    heads = 0
+    t0 = time.perf_counter()
+    while heads == 0 or time.perf_counter() - t0 < budget_s:
+        h = heads % wl.n_q
+        WQ, WK = head_slices(wq, wk, h, wl.n_kv, wl.head_dim)
+        dense_power_iteration(interaction_matrix(WQ, WK), v0[h], n_iter)
+        heads += 1
+    dt = time.perf_counter() - t0
+    return {"value": heads * n_iter / dt, "unit": "heads·iters/s",
+            "sample": f"{heads} heads of layer 0, M formed ({wl.d_model} x {wl.d_model} float64) and "
+                      f"{n_iter} dense iterations each, {dt:.1f} s"}
+
+
 def cpu_baseline_layer(wl, budget_s: float, n_iter: int):
     """The oracle's paper-literal layer estimator on host cores, layer 0 repeated."""
     from threadpoolctl import threadpool_info
@@ -528,6 +555,8 @@ def main():
         out["context"] = context_lines(args, flags)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = (cpu_baseline_layer if layer else cpu_baseline)(wl, args.cpu_seconds, n_iter)
+        if not layer and not gram and not args.no_extras:
+            out.setdefault("context", {})["oracle_explicit_M"] = cpu_explicit_m(wl, args.cpu_seconds / 3, n_iter)
     print(json.dumps(out), flush=True)
 
 

@@ -36,10 +36,13 @@ enum { PH_INIT = 0, PH_Q = 1, PH_K = 2, PH_EK = 3, PH_EQ = 4 };
 enum { LM_ROWS = 0, LM_COLS = 1 };
 
 struct Work {
-  float* zp;         // [2][H][Sk][DH]  W_K-sweep partials of z, by step parity
-  float* zn;         // [2][H][Sk]      ... and of ||v'||^2 (||v||^2 for the first sweep)
-  float* yp;         // [H][Sq][DH]     W_Q-sweep partials of y
-  float* yn;         // [H][Sq]         ... and of ||u'||^2 = sigma^2
+  // S below is the strip count of the sweep that wrote the partials (its
+  // s_out): fixed, except in the compacted launches of tolerance mode; the
+  // buffers hold the largest count the plan can use.
+  float* zp;         // [2][H][S][DH]   W_K-sweep partials of z, by step parity
+  float* zn;         // [2][H][S]       ... and of ||v'||^2 (||v||^2 for the first sweep)
+  float* yp;         // [H][S][DH]      W_Q-sweep partials of y
+  float* yn;         // [H][S]          ... and of ||u'||^2 = sigma^2
   float* sig;        // [2][H]          sigma of the last two steps
   float* vnorm0;     // [H]             ||v|| of the start vector
   int32_t* alive;    // [2][H]          head continues after the step of that parity

@@ -157,6 +157,8 @@ TAIL_CASES = [
     ("gqa8-bf16-dh64-valu", dict(n_layers=3, d_model=1024, n_q=16, n_kv=2, head_dim=64), SN_FLAG_VALU_K_SWEEP),
     ("gqa12-bf16-dh128", dict(n_layers=2, d_model=512, n_q=24, n_kv=2, head_dim=128), 0),
     ("mha-f32-dh32", dict(n_layers=2, d_model=256, n_q=8, n_kv=8, head_dim=32, dtype="f32"), 0),
+    # a cap of 40 steps, reached inside the compacted launches by the slowest heads
+    ("gqa8-bf16-dh64-cap40", dict(n_layers=3, d_model=1024, n_q=16, n_kv=2, head_dim=64, cap=40), 0),
 ]
 
 
@@ -188,7 +190,9 @@ def test_tolerance_tail_every_head(name, over, flags):
     """Tolerance mode once most heads have stopped: the sweeps then launch
     only the running heads (and the W_K units holding one), with other strip
     counts.  Every head is held to the oracle: sigma of its stopping step,
-    the stopping rule, and v, u of that step."""
+    the stopping rule (or the cap), and v, u of that step."""
+    over = dict(over)
+    cap = over.pop("cap", 400)
     wl = WORKLOADS["llama2-70b-perstep"].replace(key=name, **over)
     wq, wk, v0, gq, gk = _cpu_case(wl)
     est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=1e-4,
@@ -196,7 +200,7 @@ def test_tolerance_tail_every_head(name, over, flags):
     est.profile(True)
     v = v0.cuda().contiguous()
     u = torch.empty_like(v)
-    sigma, scale, iters = est.step(gq, gk, v, 400, u=u)
+    sigma, scale, iters = est.step(gq, gk, v, cap, u=u)
     torch.cuda.synchronize()
     prof = est.profile_read()
     est.close()
@@ -206,13 +210,13 @@ def test_tolerance_tail_every_head(name, over, flags):
     H = it.size
     expect = any(0 < int((it > k).sum()) <= H // 2 for k in POLLS if k < it.max())
     assert (prof["tail_lists"][1] >= 1) == expect, (prof["tail_lists"], expect)
-    assert it.min() >= 2 and it.max() < 400
+    assert it.min() >= 2 and it.max() <= cap
     worst = 0.0
     for l in range(wl.n_layers):
         for h in range(wl.n_q):
             WQ, WK = head_slices(_np(wq)[l], _np(wk)[l], h, wl.n_kv, wl.head_dim)
             vs = v0[l, h].double().numpy()
-            _, e = _check_tolerance_stop(it[l, h], sigma[l, h], WQ, WK, vs, 1e-4, 400)
+            _, e = _check_tolerance_stop(it[l, h], sigma[l, h], WQ, WK, vs, 1e-4, cap)
             r = power_iteration(WQ, WK, vs, int(it[l, h]))
             dv = np.linalg.norm(v[l, h] - r.v)
             du = np.linalg.norm(u[l, h] - r.u)

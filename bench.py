@@ -75,13 +75,40 @@ def copy_reference(nbytes: int):
     print(json.dumps({"mode": "copy", "bytes_read": nbytes, "bytes_written": nbytes}), flush=True)
 
 
+def code_tokens(text: str) -> str:
+    """C++ source with comments removed and every run of whitespace made one
+    space: an edit of a comment or of layout leaves it unchanged."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c in "\"'":  # string or character literal, kept whole
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+            out.append(" ")
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
 def source_hash() -> str:
-    """Hash of every kernel source and header: the counters are void once any changes."""
+    """Hash of the code (comments and layout aside) of every kernel source and
+    header: the counters are void once any of it changes."""
     h = hashlib.sha256()
     for name in sorted(os.listdir(KERNEL_DIR)):
         if name.endswith((".hip", ".h", ".cpp")):
-            with open(os.path.join(KERNEL_DIR, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+            with open(os.path.join(KERNEL_DIR, name), encoding="utf-8") as f:
+                h.update(name.encode() + b"\0" + code_tokens(f.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -230,10 +230,12 @@ def cpu_baseline_fp8(wl, budget_s: float, seq: int):
 
 
 def context_lines(args, flags: int) -> dict:
-    """Two calls reported beside the headline (context, not the metric):
-    n_iter = 1 from cold vectors (one pure stream of W_K, W_Q, W_K), and the
-    per-step scenario of Sec. 5.1: planted 0.98-gap spectra iterated to
-    tolerance 1e-4 (untimed), weights perturbed, then one timed warm call."""
+    """Calls reported beside the headline (context, not the metric): n_iter
+    = 1 from cold vectors (one pure stream of W_K, W_Q, W_K); for the sweep
+    chain, the Gram form on the same weights and iteration count; and the
+    per-step scenario of Sec. 5.1 (planted 0.98-gap spectra iterated to
+    tolerance 1e-4 untimed, weights perturbed, then one timed warm call), in
+    the chosen form and, for the chain, in the Gram form too."""
     import torch
 
     from paper_2602_18851_amd import Spectral
@@ -259,10 +261,45 @@ def context_lines(args, flags: int) -> dict:
     out["n_iter_1"] = {"ms": ms, "heads_iters_per_s": H / (ms * 1e-3),
                        "effective_GBps": (q_bytes + 2 * k_bytes + 12 * wl.d_model * H) / (ms * 1e-3) / 1e9}
     est.close()
+
+    from paper_2602_18851_amd.spectral import SN_FLAG_GRAM
+    if not flags & SN_FLAG_GRAM and wl.head_dim >= 16:
+        # the Gram form on the same weights and iteration count: the same
+        # iterates through d_h x d_h Gram matrices, weights read about four
+        # times per call instead of twice per iteration
+        n_iter = args.n_iter or wl.n_iter
+        est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha,
+                       flags=flags | SN_FLAG_GRAM)
+        v = start_vectors(wl, dev)
+        for _ in range(3):
+            est.step(wq, wk, v, n_iter)
+        torch.cuda.synchronize()
+        est.profile(True)
+        n = 20
+        e0.record()
+        for _ in range(n):
+            est.step(wq, wk, v, n_iter)
+        e1.record()
+        torch.cuda.synchronize()
+        prof = est.profile_read()
+        est.profile(False)
+        ms = e0.elapsed_time(e1) / n
+        g_ms, g_n = prof["gram_sweep"]
+        # every weight read once, the upper-triangle 16 x 16 blocks written once per query / key head
+        g_bytes = q_bytes + k_bytes + (H + wl.n_layers * wl.n_kv) * wl.head_dim * (wl.head_dim + 16) // 2 * 4
+        out["gram_form"] = {"ms": ms, "heads_iters_per_s": H * n_iter / (ms * 1e-3), "n_iter": n_iter,
+                            "gram_sweep_ms": g_ms / g_n,
+                            "gram_sweep_GBps": g_bytes / (g_ms / g_n * 1e-3) / 1e9,
+                            "gram_sweep_frac_of_peak": g_bytes / (g_ms / g_n * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                            "note": "SN_FLAG_GRAM on the same weights; not the headline, whose iterations each "
+                                    "stream the weights"}
+        est.close()
     del wq, wk, v
     torch.cuda.empty_cache()
 
     out["per_step_warm"] = per_step_warm(flags)
+    if not flags & SN_FLAG_GRAM:
+        out["per_step_warm_gram"] = per_step_warm(flags | SN_FLAG_GRAM)
     return out
 
 

@@ -539,13 +539,60 @@ ksweep_mfma_kernel(SweepArgs a) {
                       ? (int)((((uint32_t)(blockIdx.x * kMWaves + wv) * 2654435761u) >> 16) % (uint32_t)n_mine)
                       : 0;
   auto tile_at = [&](int i) { const int u = rot + i; return t0 + (u >= n_mine ? u - n_mine : u); };
+  // First sweep: the start-vector values of a tile's columns (lane: head
+  // s / 2, columns 32 kc + 8 g .. + 7) are requested with the tile, as two
+  // 16-byte loads per kc where v allows, and become the bf16 operand before
+  // the next tile is requested.
+  float vx[PROD1 ? 1 : KC][8];
+  const float* vrow = a.v + (size_t)(head0 + (s >> 1)) * a.d;
+  const bool v_vec = (a.d & 3) == 0 && (reinterpret_cast<uintptr_t>(a.v) & 15) == 0;
+  auto load_v = [&](int t) {
+    if constexpr (!PROD1) {
+      const int c0 = t * kMTileC;
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc) {
+        const int cb = c0 + 32 * kc + 8 * g;
+        if (v_vec && c0 + kMTileC <= a.d) {
+          float4 p0 = make_float4(0.f, 0.f, 0.f, 0.f), p1 = p0;
+          if (act_s) {
+            p0 = *reinterpret_cast<const float4*>(vrow + cb);
+            p1 = *reinterpret_cast<const float4*>(vrow + cb + 4);
+          }
+          vx[kc][0] = p0.x; vx[kc][1] = p0.y; vx[kc][2] = p0.z; vx[kc][3] = p0.w;
+          vx[kc][4] = p1.x; vx[kc][5] = p1.y; vx[kc][6] = p1.z; vx[kc][7] = p1.w;
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int col = cb + e;
+            vx[kc][e] = (act_s && col < a.d) ? vrow[min(col, a.d - 1)] : 0.f;
+          }
+        }
+      }
+    }
+  };
+
   __builtin_amdgcn_s_waitcnt(0);  // xs is read out before the first tile overwrites it
-  if (n_mine > 0) stage_issue<DH, kStreamPolicy>(rsrc, tl, (uint32_t)(tile_at(0) * 128), row_bytes, lane);
+  if (n_mine > 0) {
+    stage_issue<DH, kStreamPolicy>(rsrc, tl, (uint32_t)(tile_at(0) * 128), row_bytes, lane);
+    load_v(tile_at(0));
+  }
 #pragma unroll 1
   for (int i = 0; i < n_mine; ++i) {
     const int t = tile_at(i);
     const int c0 = t * kMTileC;
     __builtin_amdgcn_s_waitcnt(0);  // tile t is in LDS
+    bf16x8 b2[KC];
+    if (!PROD1) {  // first sweep: v' is the start vector itself
+#pragma unroll
+      for (int kc = 0; kc < KC; ++kc)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float x = vx[kc][e];
+          if (!lo_part) nrm0 = fmaf(x, x, nrm0);
+          const __bf16 h = (__bf16)x;
+          b2[kc][e] = lo_part ? (__bf16)(x - (float)h) : h;
+        }
+    }
     f32x4 d1[CB];
     if (PROD1) {
 #pragma unroll
@@ -565,7 +612,10 @@ ksweep_mfma_kernel(SweepArgs a) {
         for (int kc = 0; kc < KC; ++kc) cur[rb][kc] = stage_chunk(tl, 16 * rb + s, 4 * kc + g);
     }
     __builtin_amdgcn_s_waitcnt(0);  // the tile is read out: stage the next one
-    if (i + 1 < n_mine) stage_issue<DH, kStreamPolicy>(rsrc, tl, (uint32_t)(tile_at(i + 1) * 128), row_bytes, lane);
+    if (i + 1 < n_mine) {
+      stage_issue<DH, kStreamPolicy>(rsrc, tl, (uint32_t)(tile_at(i + 1) * 128), row_bytes, lane);
+      load_v(tile_at(i + 1));
+    }
     if (PROD2 && t >= n_full) {  // the ragged last tile: zero columns >= d
 #pragma unroll
       for (int kc = 0; kc < KC; ++kc) {
@@ -579,7 +629,6 @@ ksweep_mfma_kernel(SweepArgs a) {
       }
     }
 
-    bf16x8 b2[KC];
     if (PROD1) {
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb) {
@@ -608,18 +657,6 @@ ksweep_mfma_kernel(SweepArgs a) {
         for (int kc = 0; kc < KC; ++kc)
           b2[kc] = *reinterpret_cast<const bf16x8*>(vl + s * kMVPitch + 32 * kc + 8 * g);
       }
-    } else {  // first sweep: v' is the start vector itself
-      const float* vrow = a.v + (size_t)(head0 + (s >> 1)) * a.d;
-#pragma unroll
-      for (int kc = 0; kc < KC; ++kc)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int col = c0 + 32 * kc + 8 * g + e;
-          const float x = (act_s && col < a.d) ? vrow[min(col, a.d - 1)] : 0.f;
-          if (!lo_part) nrm0 = fmaf(x, x, nrm0);
-          const __bf16 h = (__bf16)x;
-          b2[kc][e] = lo_part ? (__bf16)(x - (float)h) : h;
-        }
     }
 
     if (PROD2) {

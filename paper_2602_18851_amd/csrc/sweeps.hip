@@ -445,7 +445,9 @@ sweep_kernel(SweepArgs a) {
 //   16 g + s holds row s of a 16-row block and 8 consecutive columns.
 //   v' (16 slots x 64 columns) goes back through LDS to reach the B-operand
 //   layout of product 2.
-// The loads of tile t + 1 are in flight while tile t is multiplied.
+// The loads of tile t + 1 are in flight while tile t is multiplied.  The
+// first sweep (v' = the start vector) has no product 1: its vector values
+// are requested together with their tile.
 constexpr int kMVPitch = kMTileC + 8;      // LDS row pitch of the split v'
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));

@@ -274,6 +274,29 @@ def test_bitwise_deterministic(form):
 
 
 @pytest.mark.parametrize("form", FORMS)
+def test_state_vectors_off_16_byte_alignment(form):
+    """v and u only need 4-byte alignment (the first sweep reads v in 16-byte
+    pieces only where it can): views 4 bytes off give the aligned run's bits."""
+    wl = WORKLOADS["llama2-70b-gqa"].replace(key="unaligned", n_layers=2, d_model=520, n_q=8, n_kv=2, n_iter=6)
+    wq, wk, v0, gq, gk = _cpu_case(wl)
+    ref = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True, flags=FORMS[form])
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, flags=FORMS[form])
+    big = torch.zeros(2 * v0.numel() + 1, dtype=torch.float32, device="cuda")
+    v = big[1:1 + v0.numel()].view_as(v0)
+    u = big[1 + v0.numel():].view_as(v0)
+    assert v.data_ptr() % 16 != 0 and u.data_ptr() % 16 != 0
+    v.copy_(v0.cuda())
+    sigma, scale, iters = est.step(gq, gk, v, wl.n_iter, u=u)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(sigma.cpu().double().numpy(), ref["sigma"])
+    np.testing.assert_array_equal(scale.cpu().double().numpy(), ref["scale"])
+    np.testing.assert_array_equal(iters.cpu().numpy(), ref["iters"])
+    np.testing.assert_array_equal(v.cpu().double().numpy(), ref["v"])
+    np.testing.assert_array_equal(u.cpu().double().numpy(), ref["u"])
+    est.close()
+
+
+@pytest.mark.parametrize("form", FORMS)
 def test_warm_start_continues_the_iteration(form):
     wl = WORKLOADS["gpt2-xl"].replace(n_layers=2, n_q=5, n_kv=5)
     wq, wk, v0, gq, gk = _cpu_case(wl)

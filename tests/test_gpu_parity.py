@@ -7,14 +7,12 @@ very weight bits and start vectors the GPU consumed; iteration counts equal
 chain (default) and the Gram form (flag SN_FLAG_GRAM), which computes the
 same iterates through the d_h x d_h Gram matrices."""
 
-import math
-
 import numpy as np
 import pytest
 import torch
 
 from oracle.power_iteration import head_slices, layer_scale, power_iteration, spectral_step as oracle_step
-from workloads import WORKLOADS, all_weights, layer_weights, perturb_master, layer_master, start_vectors
+from workloads import WORKLOADS, all_weights, start_vectors
 
 pytestmark = pytest.mark.gpu
 

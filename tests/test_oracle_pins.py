@@ -16,7 +16,7 @@ from oracle.power_iteration import (
     power_iteration_layer,
     spectral_step,
 )
-from workloads import WORKLOADS, bf16_round, layer_weights, planted_singular_values, start_vectors, tokens
+from workloads import WORKLOADS, all_weights, bf16_round, layer_weights, planted_singular_values, start_vectors, tokens
 
 
 def _orth(rng, n, k):
@@ -354,3 +354,79 @@ def test_degenerate_inputs():
     assert r.sigma == 0.0 and r.iters == -2
     np.testing.assert_allclose(r.v, v0 / np.linalg.norm(v0), rtol=0, atol=1e-15)
     assert not r.u.any()
+
+
+# ------------------------------------ per-layer reduction, auto-alpha, slack
+
+
+def test_layer_scale_takes_the_largest_head_sigma():
+    """Eq. "scale" takes sigma^(l) as the largest sigma_h of the layer (each
+    head's logits obey the interaction bound with its own sigma_h).  Planted
+    heads have exact sigma_h, a power of two apart from head to head; the
+    oracle's spectral_step, run to convergence, must give
+    scale_l = layer_scale(max_h planted sigma_h), which a mean, a min, a sum
+    or the first head's sigma would not."""
+    wl = WORKLOADS["llama2-70b-perstep"].replace(key="pin-max", cfg_id=41, n_layers=4, d_model=256, n_q=6,
+                                                 n_kv=2, head_dim=16)
+    wq, wk = all_weights(wl, "cpu")
+    v0 = start_vectors(wl, "cpu").double().numpy()
+    res = spectral_step(wq.float().numpy(), wk.float().numpy(), v0, 5000, n_kv=wl.n_kv, head_dim=wl.head_dim,
+                        alpha=wl.alpha, tol=1e-13)
+    assert res["iters"].max() < 5000
+    sig_exact = np.stack([planted_singular_values(wl, l)[:, 0] for l in range(wl.n_layers)])
+    np.testing.assert_allclose(res["sigma"], sig_exact, rtol=1e-9)
+    want = [layer_scale(sig_exact[l].max(), wl.alpha, wl.d_model, wl.head_dim) for l in range(wl.n_layers)]
+    np.testing.assert_allclose(res["scale"], want, rtol=1e-9)
+    # the planted layers separate the readings: every other reduction misses some layer by far
+    for other in (np.mean, np.min, np.sum, lambda s: s[0], np.median):
+        alt = [layer_scale(other(sig_exact[l]), wl.alpha, wl.d_model, wl.head_dim) for l in range(wl.n_layers)]
+        assert np.max(np.abs(np.array(alt) / np.array(want) - 1.0)) > 0.1
+
+
+def test_auto_alpha_order_statistics():
+    """App. M, Algorithm "Auto-alpha Calibration": alpha = Quantile_q(R) * kappa.
+    Identities any quantile obeys, on the sorted burn-in ratios: q = 0 is the
+    smallest, q = 1 the largest, q = 1/2 of an odd count the middle one; a
+    position q (n - 1) that falls between two order statistics interpolates
+    linearly between them; kappa multiplies; the order of the burn-in does
+    not matter; and with 10001 ratios P99.99 is the 10000th smallest."""
+    rng = np.random.default_rng(2024)
+    r = rng.uniform(7e-5, 3.7e-4, 101)
+    srt = sorted(r.tolist())
+    assert calibration.auto_alpha(r, 0.0) == srt[0]
+    assert calibration.auto_alpha(r, 1.0) == srt[-1]
+    assert calibration.auto_alpha(r, 0.5) == srt[50]
+    assert calibration.auto_alpha(r, 0.5, kappa=3.0) == pytest.approx(3.0 * srt[50], rel=1e-15)
+    assert calibration.auto_alpha(rng.permutation(r), 0.37) == calibration.auto_alpha(r, 0.37)
+    assert calibration.auto_alpha([0.0, 10.0], 0.25) == pytest.approx(2.5, rel=1e-15)
+    assert calibration.auto_alpha([4.0, 1.0, 2.0], 0.75) == pytest.approx(3.0, rel=1e-15)
+    big = rng.uniform(0.0, 1.0, 10001)
+    assert calibration.auto_alpha(big, 0.9999) == pytest.approx(sorted(big.tolist())[9999], rel=1e-12)
+    # all ratios equal: alpha is that ratio, whatever q
+    assert calibration.auto_alpha([3.6e-4] * 57, 0.9999) == pytest.approx(3.6e-4, rel=1e-15)
+
+
+def test_slack_ratio_is_one_at_the_interaction_bound_equality():
+    """Sec. 3.5: r = max|S| / B_max with B_max = sigma * d / sqrt(d_h) (the
+    interaction bound at ||x|| = sqrt(d)).  Prop. "Interaction bound" is tight
+    at x_i = sqrt(d) u_1, x_j = sqrt(d) v_1 (top singular pair of M), so the
+    brute-force logit there gives r = 1 exactly; x_i = sqrt(d) u_2 gives
+    sigma_2 / sigma_1; tokens on the sqrt(d)-sphere give r <= 1."""
+    rng = np.random.default_rng(77)
+    d, dh = 48, 8
+    WQ, WK = rng.standard_normal((d, dh)), rng.standard_normal((d, dh))
+    M = explicit.interaction_matrix(WQ, WK)
+    U, s, Vt = np.linalg.svd(M)
+    sq = math.sqrt(d)
+
+    def logit(xi, xj):
+        return float(xi @ M @ xj) / math.sqrt(dh)
+
+    assert calibration.slack_ratio(abs(logit(sq * U[:, 0], sq * Vt[0])), s[0], d, dh) == pytest.approx(1.0, rel=1e-12)
+    assert calibration.slack_ratio(abs(logit(sq * U[:, 1], sq * Vt[1])), s[0], d, dh) == pytest.approx(
+        s[1] / s[0], rel=1e-12)
+    x = rng.standard_normal((64, d))
+    x *= sq / np.linalg.norm(x, axis=1, keepdims=True)
+    S = x @ M @ x.T / math.sqrt(dh)
+    r = calibration.slack_ratio(np.abs(S).max(), s[0], d, dh)
+    assert 0.0 < r <= 1.0

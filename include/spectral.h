@@ -76,9 +76,9 @@ typedef struct {
   float r_max;         /* largest finite FP8 magnitude, 448 for OCP E4M3          */
   float tol;           /* 0: run exactly n_iter iterations.  > 0: stop a head
                           after step k >= 2 once |sigma_k - sigma_{k-1}| <=
-                          tol * sigma_k, with n_iter as the cap.  The workspace
-                          then also holds the partials of the compacted sweeps
-                          (up to one strip per 4 column tiles per head; 254 MB
+                          tol * sigma_k, with n_iter as the cap.  With
+                          head_dim >= 16 the workspace then also holds the
+                          Gram matrices of the tail (see spectral_step; 240 MB
                           at 80 x 64 heads of d_h 128, d 8192).                   */
   int32_t q_strips;    /* column strips per head in the W_Q sweep; 0 = automatic  */
   int32_t k_strips;    /* column strips per KV head in the W_K sweep; 0 = auto    */
@@ -115,9 +115,10 @@ typedef struct {
 typedef struct sn_ctx sn_ctx;
 
 /* Creates a context for one model shape on the current HIP device and
- * allocates its workspace.  hip_stream is a hipStream_t (NULL = the default
- * stream) on which every later spectral_step is queued.  On success *ctx
- * receives the handle.  Errors: SN_ENULL, SN_EINVAL, SN_EDTYPE, SN_EHIP. */
+ * allocates its workspace and a device table of the layer pointers.
+ * hip_stream is a hipStream_t (NULL = the default stream) on which every
+ * later spectral_step is queued.  On success *ctx receives the handle.
+ * Errors: SN_ENULL, SN_EINVAL, SN_EDTYPE, SN_EHIP. */
 SN_API int spectral_init(sn_ctx** ctx, const sn_shape* shape, const sn_params* params,
                          void* hip_stream);
 
@@ -140,16 +141,23 @@ SN_API int spectral_init(sn_ctx** ctx, const sn_shape* shape, const sn_params* p
  *              -1 if the start vector is zero or not finite (sigma = NaN,
  *              v unchanged, u = 0); -2 if M v = 0 (sigma = 0, v normalised
  *              start vector, u = 0).
- * The call is queued asynchronously on the context's stream.  With tol > 0
- * it waits on the stream at iterations 2, 3, 4, 6, 9, ... to stop queueing
- * once every head has converged (not in the Gram form, which never waits);
- * after a wait that finds at most half the heads running, the sweeps visit
- * only the heads that still ran there.
- * The first call with a new set of weight pointers uploads them to a device
- * table (hipMemcpyAsync from pinned memory); a call with the same pointers as
- * the previous one, in either form with tol == 0, queues kernel launches
- * only and can be captured into a HIP graph.  Weights and vectors must not
- * alias the outputs.  Errors: SN_ENULL, SN_EINVAL, SN_EHIP. */
+ * The call is queued asynchronously on the context's stream and never waits
+ * on the host.  With tol > 0 and head_dim >= 16, the first two steps (the
+ * fewest the stopping rule allows) run as sweeps over all heads; then one
+ * fixed sequence of launches lists the heads still running on the device,
+ * forms their Gram matrices G_Q = Q_h Q_h^T and G_K = K_j K_j^T (see
+ * SN_FLAG_GRAM), continues their iteration in d_h-space to the tolerance or
+ * the cap, and maps the last vectors back to v (and u) with sweeps over the
+ * listed heads only; the iterates are those of the sweeps up to rounding.
+ * (With head_dim 8 every step runs as sweeps over all heads; stopped heads
+ * leave them at once.)  The layer pointers reach the kernels through a
+ * device table written by a small kernel whose launch arguments carry them:
+ * an eager call rewrites it only when the pointers change; a call being
+ * captured into a HIP graph always writes its own copy, so every replay
+ * uses the pointers of its capture (graphs captured from one context must
+ * not replay concurrently).  Every form and mode can be captured.  Weights
+ * and vectors must not alias the outputs.  Errors: SN_ENULL, SN_EINVAL,
+ * SN_EHIP. */
 SN_API int spectral_step(sn_ctx* ctx, const void* const* wq_layers, const void* const* wk_layers,
                          float* v, float* u, int32_t n_iter, float* sigma, float* scale,
                          int32_t* iters);
@@ -207,10 +215,12 @@ SN_API int spectral_step_layer(sn_ctx* ctx, const void* const* wq_layers, const 
  *              (16-byte aligned): E4M3 codes of S~, row i, column j.
  *   max_abs    device float32 [n_layers][n_q]: max |S~| per head.
  *   n_over     device int32 [n_layers][n_q]: #{(i, j): |S~_ij| > 448}.
+ * A scaled logit that is not finite (a NaN or zero scale) counts as an
+ * overflow and makes max_abs non-finite (NaN for a NaN scale).
  * Queued on the context's stream; allocates nothing; seq_len <= 46340.
- * The layer pointer table is copied into the workspace from host memory
- * with hipMemcpyAsync (staged before the call returns), so the call is not
- * meant for stream capture.
+ * The layer pointer table is written into the workspace by a kernel whose
+ * launch arguments carry the pointers, so the call can be captured into a
+ * HIP graph.
  * Errors: SN_ENULL, SN_EINVAL, SN_EDTYPE, SN_ESTATE. */
 SN_API int spectral_logits_workspace_bytes(const sn_shape* shape, int32_t seq_len, int64_t* bytes);
 SN_API int spectral_logits_fp8(sn_ctx* ctx, const void* const* x_layers, int64_t ld_x, int32_t seq_len,
@@ -218,9 +228,9 @@ SN_API int spectral_logits_fp8(sn_ctx* ctx, const void* const* x_layers, int64_t
                                void* workspace, int64_t workspace_bytes, uint8_t* codes, float* max_abs,
                                int32_t* n_over);
 
-/* Redirects later calls to another hipStream_t.  Unless that stream is being
- * captured, it is first made to wait for the context's last upload of the
- * weight-pointer table (queued on the previous stream). */
+/* Redirects later calls to another hipStream_t.  Unless either stream is
+ * being captured, the new stream is first made to wait for all work queued
+ * on the previous one (they share the workspace and the pointer table). */
 SN_API int spectral_set_stream(sn_ctx* ctx, void* hip_stream);
 
 /* Frees the context and its workspace (waits for its queued work first). */

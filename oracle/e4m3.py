@@ -58,5 +58,8 @@ def encode(x, saturate: bool = False) -> np.ndarray:
 
 
 def overflows(x, r_max: float = R_MAX) -> np.ndarray:
-    """The paper's overflow predicate |x| > R_max for an already-scaled value."""
-    return np.abs(np.asarray(x, dtype=np.float64)) > r_max
+    """The paper's overflow predicate |x| > R_max for an already-scaled value.
+    A value that is not finite (NaN, inf: e.g. logits scaled by a NaN or zero
+    scale) is not representable either and counts as an overflow, the outcome
+    the predicate exists to flag (Sec. 1: an overflow yields NaN or inf)."""
+    return ~(np.abs(np.asarray(x, dtype=np.float64)) <= r_max)

@@ -37,7 +37,13 @@ __host__ __device__ constexpr int tri_index(int bi, int bj) {  // bj >= bi
 
 template <typename T, int DH>
 __global__ void __launch_bounds__(64 * kGWaves) __attribute__((amdgpu_waves_per_eu(DH >= 128 ? 2 : 4)))
-gram_kernel(GramArgs a) {
+gram_kernel(GramArgs args) {
+  GramArgs a = args;
+  if (a.ctl) {  // tail: the listed units, with the count and strips chosen on the device
+    a.s_g = uni(a.ctl[TC_GRAM + 1]);
+    a.tps = uni(a.ctl[TC_GRAM + 2]);
+    a.n_items = uni(a.ctl[TC_GRAM]) * a.s_g;
+  }
   constexpr int ES = sizeof(T);
   constexpr int RB = DH / 16;
   constexpr int NB = RB * (RB + 1) / 2;
@@ -48,7 +54,7 @@ gram_kernel(GramArgs a) {
   const int q = lane >> 4, s = lane & 15;
   const int item = blockIdx.x * kGWaves + wv;
   if (item >= a.n_items) return;
-  const int unit = item / a.s_g, strip = item % a.s_g;
+  const int unit = a.list ? uni(a.list[item / a.s_g]) : item / a.s_g, strip = item % a.s_g;
   int layer, row0, tab;
   if (unit < a.H) {
     layer = unit / a.n_q;
@@ -236,36 +242,50 @@ __global__ void __launch_bounds__(IterShape<DH>::NT) gram_iterate_kernel(IterArg
   __shared__ float gl[DH * (DH + 1)];
   __shared__ float wb[DH], tb[DH];
   __shared__ float red_a[NW], red_b[NW];
-  const int h = blockIdx.x, t = threadIdx.x, lane = t & 63, wv = t >> 6;
+  const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
   const int R = t >> 4, C = t & 15;
+  // the head, and the Gram items of its query and key matrices
+  int h = blockIdx.x, s_g = a.s_g;
+  if (a.list) {
+    const int nq = uni(a.ctl[TC_NQ]);
+    if ((int)blockIdx.x >= nq) return;
+    h = uni(a.list[blockIdx.x]);
+    s_g = uni(a.ctl[TC_GRAM + 1]);
+  }
   const int layer = h / a.n_q;
   const int j = layer * a.n_kv + (h % a.n_q) / a.g;
+  const int item_q = a.list ? (int)blockIdx.x : h;
+  const int item_k = a.list ? uni(a.ctl[TC_NQ]) + uni(a.kvpos[j]) : a.H + j;
 
-  // start vector: ||v||^2 and z = K_j v from the first W_K sweep (slot 0)
+  // z of step k0 + 1: K_j v' / ||v'|| from the partials of the W_K sweep of
+  // step k0 (slot k0 & 1; at k0 = 0 the first sweep, v' = the start vector)
+  const int slot = a.k0 & 1;
   float nv2 = 0.f;
-  for (int st = 0; st < a.s_k; ++st) nv2 += a.w.zn[(size_t)h * a.s_k + st];
-  if (t == 0) a.w.vnorm0[h] = sqrtf(nv2);
-  if (!(nv2 > 0.f) || !isfinite(nv2)) {
-    if (t == 0) {
-      a.sigma[h] = __builtin_nanf("");
-      a.iters[h] = -1;
+  for (int st = 0; st < a.s_k; ++st) nv2 += a.w.zn[((size_t)slot * a.H + h) * a.s_k + st];
+  if (a.k0 == 0) {
+    if (t == 0) a.w.vnorm0[h] = sqrtf(nv2);
+    if (!(nv2 > 0.f) || !isfinite(nv2)) {
+      if (t == 0) {
+        a.sigma[h] = __builtin_nanf("");
+        a.iters[h] = -1;
+      }
+      return;
     }
-    return;
   }
   const float inv0 = 1.0f / sqrtf(nv2);
   if (t < DH) {
     float z = 0.f;
-    for (int st = 0; st < a.s_k; ++st) z += a.w.zp[((size_t)h * a.s_k + st) * DH + t];
+    for (int st = 0; st < a.s_k; ++st) z += a.w.zp[(((size_t)slot * a.H + h) * a.s_k + st) * DH + t];
     tb[t] = z * inv0;
   }
   float gq[RPT][CPT], gk[RPT][CPT];
-  gram_to_regs<DH>(a.gp + (size_t)h * a.s_g * S::NB * 256, a.s_g, gl, gq);
-  gram_to_regs<DH>(a.gp + (size_t)(a.H + j) * a.s_g * S::NB * 256, a.s_g, gl, gk);
+  gram_to_regs<DH>(a.gp + (size_t)item_q * s_g * S::NB * 256, s_g, gl, gq);
+  gram_to_regs<DH>(a.gp + (size_t)item_k * s_g * S::NB * 256, s_g, gl, gk);
 
-  float zscale = 1.f, prev = 0.f;
+  float zscale = 1.f, prev = a.k0 > 0 ? a.w.sig[(size_t)slot * a.H + h] : 0.f;
   float out[RPT];
 #pragma unroll 1
-  for (int k = 1;; ++k) {
+  for (int k = a.k0 + 1;; ++k) {
     // w = G_Q z with z = zscale * tb; lane C == 0 of row band R owns rows RPT R ..
     gram_matvec<RPT, CPT>(gq, tb, C, out);
     float part = 0.f;

@@ -18,6 +18,7 @@ constexpr int kMaxGC = 8;             // query heads per W_K work item
 constexpr int kQTargetItems = 10240;  // wave work items aimed for in a W_Q sweep
 constexpr int kMinTilesPerStrip = 4;  // automatic strips: at least this many tiles per wave
 constexpr int kTailMinTiles = 4;      // ... in the compacted launches of the tolerance-mode tail
+constexpr int kTailSteps = 2;         // tolerance mode: full sweep steps before the tail (the rule's minimum)
 constexpr int kSetupUnroll = 4;       // producer partials summed per round in a sweep's set-up
 constexpr int kKTargetItems = 4096;   // ... and in a W_K sweep (register-heavier waves)
 constexpr int kKMfmaResident = 2048;  // waves of the matrix-core W_K sweep resident at once (256 CUs x 8)
@@ -35,9 +36,20 @@ constexpr int kRedThreads = 512;
 enum { PH_INIT = 0, PH_Q = 1, PH_K = 2, PH_EK = 3, PH_EQ = 4 };
 enum { LM_ROWS = 0, LM_COLS = 1 };
 
+// Control block of the tolerance-mode tail, written on the device by the
+// list kernel: for each compacted launch the number of listed entries and
+// the strips (and tiles per strip) chosen for that count.
+enum {
+  TC_GRAM = 0,   // Gram sweep over the running query heads, then their key heads
+  TC_EK = 3,     // final W_K sweep over the W_K units holding a running head
+  TC_EQ = 6,     // final W_Q sweep over the running query heads
+  TC_NQ = 9,     // running query heads (the first entries of the Gram list)
+  TC_WORDS = 10
+};
+
 struct Work {
   // S below is the strip count of the sweep that wrote the partials (its
-  // s_out): fixed, except in the compacted launches of tolerance mode; the
+  // s_out): fixed, except in the final sweeps of the tolerance-mode tail; the
   // buffers hold the largest count the plan can use.
   float* zp;         // [2][H][S][DH]   W_K-sweep partials of z, by step parity
   float* zn;         // [2][H][S]       ... and of ||v'||^2 (||v||^2 for the first sweep)
@@ -46,11 +58,14 @@ struct Work {
   float* sig;        // [2][H]          sigma of the last two steps
   float* vnorm0;     // [H]             ||v|| of the start vector
   int32_t* alive;    // [2][H]          head continues after the step of that parity
-  int32_t* n_alive;  // [2]             heads still running after a W_K sweep
   int32_t* iters;    // [H]             used when the caller passes no iters array
-  float* fin;        // [H][2][DH]      Gram form: z and y of each head's last step
+  float* fin;        // [H][2][DH]      Gram form and tail: z and y of each head's last step
   int32_t* zs;       // [H]             tolerance mode: strips of each head's last ||v'||^2 partials
-  int32_t* list;     // [H + U]         tolerance-mode tail: running query heads, then running W_K units
+  int32_t* list_g;   // [H + L n_kv]    tail: running query heads, then their key heads (H + index)
+  int32_t* list_k;   // [U]             tail: W_K units holding a running head
+  int32_t* kvpos;    // [L n_kv]        tail: place of a key head among the listed key heads, or -1
+  int32_t* ctl;      // [TC_WORDS]      tail control block
+  float* zt;         // [H][S_t]        tail: ||v'||^2 partials of the final W_K sweep
 };
 
 struct SweepArgs {
@@ -61,7 +76,9 @@ struct SweepArgs {
   int32_t s_out, tps, n_tiles, nch, n_items;
   int32_t k, n_iter, want_vec;
   float tol;
-  const int32_t* list;      // tail launches: the decoded unit of item index r is list[r] (-1: none)
+  const int32_t* list;      // tail launches: the decoded unit of item index r is list[r]
+  const int32_t* ctl;       // tail launches: count, strips, tiles per strip at ctl[0..2] (else nullptr)
+  const int32_t* only;      // final sweeps of the tail: a head takes part only if only[head] != 0
   Work w;
   float* v;
   float* u;
@@ -73,6 +90,8 @@ struct FinArgs {
   int32_t H, L, n_q, d, s_k;
   int32_t slot_fixed;  // workspace slot of the ||v'||^2 partials; -1: parity of the last step
   const int32_t* zs;   // per-head strips of those partials, or nullptr: s_k for every head
+  const int32_t* tail; // tolerance mode: flags of the heads the tail finished (else nullptr) ...
+  const float* zt;     // ... whose ||v'||^2 partials are zt[head][zs[head]]
   float coef;
   Work w;
   float* v;
@@ -88,13 +107,23 @@ struct GramArgs {
   int64_t ld;
   int32_t d, L, n_q, n_kv, H;
   int32_t s_g, tps, n_tiles, n_items;
-  float* gp;  // [units][s_g][NB][64 lanes][4]: partial Gram blocks in the MFMA output layout
+  const int32_t* list;      // tail: unit of list entry r is list[r]; count and strips in ctl (else nullptr)
+  const int32_t* ctl;
+  float* gp;  // [items][NB][64 lanes][4]: partial Gram blocks in the MFMA output layout, item = entry * s_g + strip
 };
 
+// The d_h-space iteration.  The Gram form starts at step 1 from the first W_K
+// sweep's z partials (slot 0); the tolerance-mode tail continues the heads
+// still running after step k0 of the sweep chain from that step's partials
+// (slot k0 & 1) and sigma_{k0}, one workgroup per listed head.
 struct IterArgs {
   int32_t H, n_q, n_kv, g, s_k, s_g, n_iter;
+  int32_t k0;               // steps already taken
   float tol;
   const float* gp;
+  const int32_t* list;      // tail: Gram list, its count of query heads in ctl (else nullptr)
+  const int32_t* ctl;
+  const int32_t* kvpos;
   Work w;
   float* sigma;
   int32_t* iters;
@@ -167,12 +196,16 @@ struct LayerFinArgs {
 void launch_sweep(bool bf16, int head_dim, int ph, int gc, bool mfma, int n_items, hipStream_t st,
                   const SweepArgs& a);
 void launch_finalize(int blocks, hipStream_t st, const FinArgs& f);
-// Lists the heads still running after the W_K sweep of parity `slot` in
-// list_q[0 .. H) and the W_K units holding one of them in list_k[0 ..
-// n_units), both ascending and padded with -1, and clears the other parity's
-// flag of every stopped head.  One workgroup.
-void launch_tail_lists(const SweepArgs& a, int slot, int gc, int n_units, int32_t* list_q, int32_t* list_k,
-                       hipStream_t st);
+// Tail of tolerance mode after step k of the chain (running flags of parity
+// k & 1): lists the running query heads, then the key heads serving one of
+// them (Gram list), and the W_K units holding one, all ascending; the place
+// of each listed key head; and the counts and strips of the tail's launches
+// (TailPlan) in the control block.  One workgroup.
+struct TailPlan {
+  int32_t n_tiles_g, n_tiles_k, n_tiles_q;   // column tiles of the Gram, W_K and W_Q sweeps
+  int32_t target_g, target_k, target_q;      // wave items aimed for in each
+};
+void launch_tail_lists(const SweepArgs& a, int slot, int gc, int n_units, const TailPlan& tp, hipStream_t st);
 void launch_gram(bool bf16, int head_dim, int n_items, hipStream_t st, const GramArgs& g);
 void launch_gram_iterate(int head_dim, int heads, hipStream_t st, const IterArgs& a);
 void launch_layer_sweep(bool bf16, int head_dim, int mode, int n_items, hipStream_t st, const LayerArgs& a);

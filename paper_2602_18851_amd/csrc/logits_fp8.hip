@@ -239,8 +239,12 @@ __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
   // S~ = (q . k) / (sqrt(d_h) scale), the factor formed in double
   const float c = (float)(1.0 / (std::sqrt((double)DH) * (double)a.scale[layer]));
   const bool words = (a.seq & 3) == 0;  // rows start 4-byte aligned
+  // A scaled logit that is not finite (a NaN or zero scale, an inf product)
+  // cannot be represented either: it counts as an overflow, and the maximum
+  // is kept on the bit patterns of |S~| (ordered as integers, +inf and NaN
+  // above every finite value), so a NaN or inf reaches max_abs.
   int n_over = 0;
-  float mx = 0.f;
+  int mx = 0;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = i0 + 16 * i + s;
@@ -253,8 +257,8 @@ __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
         v[e] = acc[i][j][e] * c;
         const bool in = row < a.seq && col + e < a.seq;
         const float av = fabsf(v[e]);
-        n_over += (in && av > 448.f) ? 1 : 0;
-        mx = in ? fmaxf(mx, av) : mx;
+        n_over += (in && !(av <= 448.f)) ? 1 : 0;
+        mx = in ? max(mx, __float_as_int(av)) : mx;
       }
       if (a.codes && row < a.seq) {
         int w = __builtin_amdgcn_cvt_pk_fp8_f32(v[0], v[1], 0, false);
@@ -270,17 +274,17 @@ __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
       }
     }
   }
-  // per-head statistics: integer sum and maximum of non-negative floats are
-  // independent of the order of the atomics
+  // per-head statistics: integer sum and integer maximum of the bit patterns
+  // of non-negative floats are independent of the order of the atomics
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) {
     n_over += __shfl_xor(n_over, m);
-    mx = fmaxf(mx, __shfl_xor(mx, m));
+    mx = max(mx, __shfl_xor(mx, m));
   }
   if (lane == 0) {
     const int hl = layer * a.n_heads + h;
     if (n_over) atomicAdd(a.n_over + hl, n_over);
-    atomicMax(reinterpret_cast<int32_t*>(a.max_abs) + hl, __float_as_int(mx));
+    atomicMax(reinterpret_cast<int32_t*>(a.max_abs) + hl, mx);
   }
 }
 

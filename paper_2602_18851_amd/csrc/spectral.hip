@@ -56,16 +56,18 @@ struct Plan {
   int tile_cq, n_tiles_q;                    // W_Q sweep
   bool mfma_k;  // W_K sweeps on the matrix cores
   int s_q, tps_q, s_k, tps_k;
-  bool tail;    // tolerance mode of the default form: compacted launches once few heads run
-  int s_qmax, s_kmax;  // most strips any sweep of the plan writes (workspace sizing)
+  bool tail;    // tolerance mode of the default form: the heads still running after the first
+                // steps are finished in d_h-space (needs d_h >= 16)
+  int s_tmax;   // most strips of the tail's final W_K sweep
   bool gram;    // Gram form
   int units_g, s_g, tps_g, n_tiles_g, nb_g;
+  int g_items;  // Gram partial items the workspace holds
   bool layer;   // layer-level form
   int s_lq, tps_lq, s_lk, tps_lk;  // strips of the layer-form row sweeps over W_Q and W_K
   int rs_q, rbp_q, rs_k, rbp_k;    // row splits (and row blocks per split) of its column sweeps
-  size_t off_zp, off_zn, off_yp, off_yn, off_sig, off_vn, off_alive, off_nalive, off_iters, off_fin, off_gp;
+  size_t off_zp, off_zn, off_yp, off_yn, off_sig, off_vn, off_alive, off_iters, off_fin, off_gp;
   size_t off_lz, off_ly, off_lvin, off_lcol, off_lu, off_lv, off_ln2, off_ln2p, off_lstat;
-  size_t off_zs, off_list;
+  size_t off_zs, off_lg, off_lk, off_kvpos, off_ctl, off_zt;
   size_t bytes;
 };
 
@@ -139,22 +141,20 @@ Plan make_plan(const sn_shape* s, const sn_params* p) {
   strips(pl.n_tiles, (int64_t)s->n_layers * s->n_kv_heads * pl.nch, p->k_strips,
          pl.mfma_k ? kKMfmaResident : kKTargetItems, pl.mfma_k, &pl.s_k, &pl.tps_k);
   pl.gram = (p->flags & SN_FLAG_GRAM) != 0;
-  // Tolerance mode: once at most half the heads still run, the sweeps launch
-  // the running heads (and the W_K units holding one) only, with strips
-  // chosen for that count; the buffers hold the most strips strips() gives.
-  pl.tail = p->tol > 0.f && !pl.gram;
-  pl.s_qmax = pl.s_q;
-  pl.s_kmax = pl.s_k;
-  if (pl.tail) {
-    pl.s_qmax = std::max(pl.s_q, std::max(1, pl.n_tiles_q / kTailMinTiles));
-    pl.s_kmax = std::max(pl.s_k, std::max(1, pl.n_tiles / kTailMinTiles));
-  }
-  if (pl.gram) {
+  // Tolerance mode: after the first kTailSteps steps, the heads still running
+  // are listed on the device and finished in d_h-space through their Gram
+  // matrices, formed for the listed heads only; strips of those launches are
+  // chosen on the device for the listed count (at most max(count, target)
+  // items each).
+  pl.tail = p->tol > 0.f && !pl.gram && dh >= 16;
+  pl.s_tmax = std::max(1, pl.n_tiles / kTailMinTiles);
+  if (pl.gram || pl.tail) {
     const int rb = dh / 16;
     pl.nb_g = rb * (rb + 1) / 2;
     pl.units_g = pl.H + s->n_layers * s->n_kv_heads;
     pl.n_tiles_g = ceil_div((int64_t)s->d_model * esize(s->dtype), 128);
     strips(pl.n_tiles_g, pl.units_g, 0, kGTargetItems, true, &pl.s_g, &pl.tps_g);
+    pl.g_items = pl.gram ? pl.units_g * pl.s_g : std::max(pl.units_g, kGTargetItems);
   }
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -163,22 +163,26 @@ Plan make_plan(const sn_shape* s, const sn_params* p) {
     return o;
   };
   const size_t H = pl.H;
-  pl.off_zp = take(2 * H * pl.s_kmax * dh * 4);
-  pl.off_zn = take(2 * H * pl.s_kmax * 4);
-  pl.off_yp = take(H * pl.s_qmax * dh * 4);
-  pl.off_yn = take(H * pl.s_qmax * 4);
+  pl.off_zp = take(2 * H * pl.s_k * dh * 4);
+  pl.off_zn = take(2 * H * pl.s_k * 4);
+  pl.off_yp = take(H * pl.s_q * dh * 4);
+  pl.off_yn = take(H * pl.s_q * 4);
   pl.off_sig = take(2 * H * 4);
   pl.off_vn = take(H * 4);
   pl.off_alive = take(2 * H * 4);
-  pl.off_nalive = take(2 * 4);
   pl.off_iters = take(H * 4);
   if (pl.tail) {
+    const size_t nkvh = (size_t)s->n_layers * s->n_kv_heads;
     pl.off_zs = take(H * 4);
-    pl.off_list = take((H + (size_t)s->n_layers * s->n_kv_heads * pl.nch) * 4);
+    pl.off_lg = take((H + nkvh) * 4);
+    pl.off_lk = take(nkvh * pl.nch * 4);
+    pl.off_kvpos = take(nkvh * 4);
+    pl.off_ctl = take(TC_WORDS * 4);
+    pl.off_zt = take(H * pl.s_tmax * 4);
   }
-  if (pl.gram) {
+  if (pl.gram || pl.tail) {
     pl.off_fin = take(H * 2 * dh * 4);
-    pl.off_gp = take((size_t)pl.units_g * pl.s_g * pl.nb_g * 256 * 4);
+    pl.off_gp = take((size_t)pl.g_items * pl.nb_g * 256 * 4);
   }
   pl.layer = (p->flags & SN_FLAG_LAYER) != 0;
   if (pl.layer) {
@@ -214,6 +218,36 @@ struct ProfRec {
   hipEvent_t a, b;
 };
 
+// Device pointer tables are written by a kernel whose arguments carry the
+// pointers: the values are taken when the launch is queued (or captured),
+// with no host buffer that must outlive the call.
+constexpr int kTabChunk = 256;
+struct TabFill {
+  const void* p[kTabChunk];
+  const void** dst;
+  int32_t n;
+};
+
+__global__ void table_fill_kernel(TabFill f) {
+  const int i = threadIdx.x;
+  if (i < f.n) f.dst[i] = f.p[i];
+}
+
+// dst[0 .. n) = src(0 .. n), in launches of up to kTabChunk pointers.
+template <typename Src>
+int fill_table(const void** dst, int n, Src src, hipStream_t st) {
+  for (int i0 = 0; i0 < n; i0 += kTabChunk) {
+    TabFill f{};
+    f.dst = dst + i0;
+    f.n = std::min(kTabChunk, n - i0);
+    for (int i = 0; i < f.n; ++i) f.p[i] = src(i0 + i);
+    table_fill_kernel<<<dim3(1), kTabChunk, 0, st>>>(f);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(SN_EHIP, std::string("table fill launch failed: ") + hipGetErrorString(e));
+  }
+  return SN_OK;
+}
+
 }  // namespace
 
 // Shared with the host-side calibration helpers (calibration.cpp).
@@ -226,12 +260,12 @@ struct sn_ctx {
   hipStream_t stream = nullptr;
   int device = 0;
   char* ws = nullptr;
+  bool owns_ws = true;
   Work w{};
-  const void** d_tab = nullptr;  // device [2L]: wq pointers then wk pointers
-  const void** h_tab = nullptr;  // pinned staging for the table copy
-  std::vector<const void*> cached;
+  const void** d_tab = nullptr;  // device [2][2L]: the eager table, then the table of captured calls
+  const void** tab = nullptr;    // the table the current call's launches read
+  std::vector<const void*> cached;  // pointers in the eager table
   hipEvent_t tab_event = nullptr;
-  int32_t* h_alive = nullptr;    // pinned readback of n_alive
   bool prof = false;
   std::vector<ProfRec> recs;
   std::vector<hipEvent_t> pool;
@@ -270,25 +304,27 @@ int timed(sn_ctx* c, int kind, F&& launch) {
   return SN_OK;
 }
 
-// Compacted launch of the tolerance-mode tail: `count` entries of `list`
-// (query heads for a W_Q sweep, W_K units otherwise), `s` strips of `tps`
-// tiles each.
+// Compacted launch of the tolerance-mode tail over the entries of `list`
+// (query heads for a W_Q sweep, W_K units otherwise); the count and strips
+// are read from `ctl` on the device, and the grid holds max_items items.
 struct TailLaunch {
   const int32_t* list = nullptr;
-  int count = 0, s = 0, tps = 0;
+  const int32_t* ctl = nullptr;
+  int max_items = 0;
 };
 
 int run_sweep(sn_ctx* c, int ph, SweepArgs a, const TailLaunch& tl = TailLaunch{}) {
+  a.ctl = tl.ctl;
   const Plan& pl = c->plan;
   const int n_units = c->shape.n_layers * c->shape.n_kv_heads * pl.nch;
   if (ph == PH_Q || ph == PH_EQ) {
-    a.mats = c->d_tab;
+    a.mats = c->tab;
     a.s_out = pl.s_q;
     a.tps = pl.tps_q;
     a.n_tiles = pl.n_tiles_q;
     a.n_items = pl.H * pl.s_q;
   } else {
-    a.mats = c->d_tab + c->shape.n_layers;
+    a.mats = c->tab + c->shape.n_layers;
     a.s_out = pl.s_k;
     a.tps = pl.tps_k;
     a.n_tiles = pl.n_tiles;
@@ -296,10 +332,7 @@ int run_sweep(sn_ctx* c, int ph, SweepArgs a, const TailLaunch& tl = TailLaunch{
   }
   if (tl.list) {
     a.list = tl.list;
-    a.s_out = tl.s;
-    a.tps = tl.tps;
-    a.n_items = tl.count * tl.s;
-    if (a.n_items == 0) return SN_OK;
+    a.n_items = tl.max_items;
   }
   const int kind = ph == PH_INIT ? KIND_INIT : ph == PH_Q ? KIND_Q : ph == PH_K ? KIND_K : KIND_EMIT;
   return timed(c, kind, [&] {
@@ -314,8 +347,17 @@ float scale_coef(const sn_ctx* c) {
                  (std::sqrt((double)c->shape.head_dim) * (double)c->params.eta_fp8 * (double)c->params.r_max));
 }
 
-// Checks the layer pointers and the device, and refreshes the device copy of
-// the per-layer pointer table when the pointers changed.
+bool capturing(hipStream_t st) {
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  return hipStreamIsCapturing(st, &cap) == hipSuccess && cap != hipStreamCaptureStatusNone;
+}
+
+// Checks the layer pointers and the device, and points the call's launches
+// at a device table of the per-layer pointers.  Eager calls share one table,
+// rewritten only when the pointers change.  A call being captured into a
+// graph always writes its pointers into a second table, so that every replay
+// restores its own pointers whatever eager calls ran in between (graphs
+// captured from one context must therefore not replay concurrently).
 int update_table(sn_ctx* c, const void* const* wq_layers, const void* const* wk_layers) {
   const int L = c->shape.n_layers;
   for (int l = 0; l < L; ++l) {
@@ -326,18 +368,21 @@ int update_table(sn_ctx* c, const void* const* wq_layers, const void* const* wk_
   int cur_dev = 0;
   SN_HIP(hipGetDevice(&cur_dev));
   if (cur_dev != c->device) return fail(SN_ESTATE, "the current HIP device is not the context's device");
+  auto src = [&](int i) { return i < L ? wq_layers[i] : wk_layers[i - L]; };
+  if (capturing(c->stream)) {
+    c->tab = c->d_tab + 2 * L;
+    return fill_table(c->tab, 2 * L, src, c->stream);
+  }
+  c->tab = c->d_tab;
   bool same = c->cached.size() == (size_t)(2 * L);
   for (int l = 0; same && l < L; ++l)
     same = c->cached[l] == wq_layers[l] && c->cached[L + l] == wk_layers[l];
   if (!same) {
-    SN_HIP(hipEventSynchronize(c->tab_event));  // the staging buffer's previous copy has been read
-    c->cached.assign(2 * L, nullptr);
-    for (int l = 0; l < L; ++l) {
-      c->h_tab[l] = c->cached[l] = wq_layers[l];
-      c->h_tab[L + l] = c->cached[L + l] = wk_layers[l];
-    }
-    SN_HIP(hipMemcpyAsync(c->d_tab, c->h_tab, 2 * L * sizeof(void*), hipMemcpyHostToDevice, c->stream));
-    SN_HIP(hipEventRecord(c->tab_event, c->stream));
+    int rc = fill_table(c->tab, 2 * L, src, c->stream);
+    if (rc != SN_OK) return rc;
+    c->cached.assign(wq_layers, wq_layers + L);
+    c->cached.insert(c->cached.end(), wk_layers, wk_layers + L);
+    if (c->tab_event) SN_HIP(hipEventRecord(c->tab_event, c->stream));
   }
   return SN_OK;
 }
@@ -347,7 +392,7 @@ int update_table(sn_ctx* c, const void* const* wq_layers, const void* const* wk_
 int layer_sweep(sn_ctx* c, bool q, int mode, LayerArgs a) {
   const Plan& pl = c->plan;
   const int L = c->shape.n_layers;
-  a.mats = c->d_tab + (q ? 0 : L);
+  a.mats = c->tab + (q ? 0 : L);
   a.ld = c->shape.ld;
   a.d = c->shape.d_model;
   a.n_tiles = pl.n_tiles_q;
@@ -403,66 +448,10 @@ int layer_reduce(sn_ctx* c, const float* col, int units, int cstride, int mode, 
                [&] { launch_layer_reduce(c->shape.n_layers, c->stream, r); });
 }
 
-// The sweeps of the default form: first W_K sweep, then n_iter x (W_Q sweep,
-// W_K sweep).  In tolerance mode the host polls the count of running heads at
-// iterations 2, 3, 4, 6, 9, ... and stops queueing once it is zero.  From a
-// poll that finds at most half the heads running, each sweep launches only
-// the heads (W_Q) and W_K units that held a running head at that poll, with
-// strips sized for their count; the lists are rebuilt at every later poll.
-// The strip count of a sweep's partials travels with them: a sweep reads its
-// producer's count (s_k or s_q of the args) and writes its own (s_out), and
-// the W_K sweep's slot stride uses its own count as well.
-int run_chain(sn_ctx* c, SweepArgs a, float* u) {
+GramArgs gram_args(const sn_ctx* c) {
   const Plan& pl = c->plan;
-  const int n_units = c->shape.n_layers * c->shape.n_kv_heads * pl.nch;
-  int rc;
-  a.k = 0;
-  if ((rc = run_sweep(c, PH_INIT, a)) != SN_OK) return rc;
-  int next_check = 2;
-  TailLaunch tq, tk;  // empty until the first compacting poll
-  for (int k = 1; k <= a.n_iter; ++k) {
-    a.k = k;
-    a.want_vec = (u != nullptr) && (c->params.tol > 0.f || k == a.n_iter);
-    if ((rc = run_sweep(c, PH_Q, a, tq)) != SN_OK) return rc;
-    a.want_vec = 0;
-    a.s_q = tq.list ? tq.s : pl.s_q;  // the strips the W_Q sweep wrote
-    a.s_k = tk.list ? tk.s : pl.s_k;  // ... and those this W_K sweep writes
-    if ((rc = run_sweep(c, PH_K, a, tk)) != SN_OK) return rc;
-    if (c->params.tol > 0.f && k == next_check && k < a.n_iter) {
-      SN_HIP(hipMemcpyAsync(c->h_alive, c->w.n_alive + (k & 1), sizeof(int32_t), hipMemcpyDeviceToHost,
-                            c->stream));
-      SN_HIP(hipStreamSynchronize(c->stream));
-      const int n = c->h_alive[0];
-      if (n == 0) break;
-      next_check = k < 4 ? k + 1 : k + k / 2;
-      if (pl.tail && n <= pl.H / 2) {
-        int32_t* list_q = c->w.list;
-        int32_t* list_k = c->w.list + pl.H;
-        rc = timed(c, KIND_TAIL, [&] { launch_tail_lists(a, k & 1, pl.gc, n_units, list_q, list_k, c->stream); });
-        if (rc != SN_OK) return rc;
-        tq.list = list_q;
-        tq.count = std::min(n, pl.H);
-        strips(pl.n_tiles_q, tq.count, 0, kQTargetItems, false, &tq.s, &tq.tps, kTailMinTiles);
-        tk.list = list_k;
-        tk.count = std::min(n, n_units);
-        strips(pl.n_tiles, tk.count, 0, pl.mfma_k ? kKMfmaResident : kKTargetItems, pl.mfma_k, &tk.s, &tk.tps,
-               kTailMinTiles);
-      }
-    }
-  }
-  return SN_OK;
-}
-
-// The Gram form of one call: first W_K sweep, Gram sweep, d_h-space
-// iteration, final W_K sweep (and W_Q sweep for u).
-int run_gram(sn_ctx* c, SweepArgs a, float* u) {
-  const Plan& pl = c->plan;
-  int rc;
-  a.k = 0;
-  if ((rc = run_sweep(c, PH_INIT, a)) != SN_OK) return rc;
-
   GramArgs g{};
-  g.mats = c->d_tab;
+  g.mats = c->tab;
   g.ld = c->shape.ld;
   g.d = c->shape.d_model;
   g.L = c->shape.n_layers;
@@ -474,10 +463,11 @@ int run_gram(sn_ctx* c, SweepArgs a, float* u) {
   g.n_tiles = pl.n_tiles_g;
   g.n_items = pl.units_g * pl.s_g;
   g.gp = reinterpret_cast<float*>(c->ws + pl.off_gp);
-  const int dh = c->shape.head_dim;
-  rc = timed(c, KIND_GRAM, [&] { launch_gram(c->shape.dtype == SN_BF16, dh, g.n_items, c->stream, g); });
-  if (rc != SN_OK) return rc;
+  return g;
+}
 
+IterArgs iter_args(const sn_ctx* c, const SweepArgs& a) {
+  const Plan& pl = c->plan;
   IterArgs it{};
   it.H = pl.H;
   it.n_q = c->shape.n_q_heads;
@@ -487,17 +477,169 @@ int run_gram(sn_ctx* c, SweepArgs a, float* u) {
   it.s_g = pl.s_g;
   it.n_iter = a.n_iter;
   it.tol = a.tol;
-  it.gp = g.gp;
+  it.gp = reinterpret_cast<const float*>(c->ws + pl.off_gp);
   it.w = c->w;
   it.sigma = a.sigma;
   it.iters = a.iters;
+  return it;
+}
+
+// Tolerance-mode tail after step k0 of the chain, as a fixed sequence of
+// launches whatever the heads do: list the heads still running (and their
+// key heads and W_K units), form the Gram matrices of the listed heads only,
+// iterate each listed head in d_h-space to the tolerance or the cap, then map
+// its last vectors back to v (and u) with final sweeps over the lists.  The
+// iterates are those the sweep chain would compute (see gram.hip); nothing is
+// read back to the host.
+int run_tail(sn_ctx* c, SweepArgs a, float* u, int k0) {
+  const Plan& pl = c->plan;
+  const int n_units = c->shape.n_layers * c->shape.n_kv_heads * pl.nch;
+  const int target_k = pl.mfma_k ? kKMfmaResident : kKTargetItems;
+  TailPlan tp{pl.n_tiles_g, pl.n_tiles, pl.n_tiles_q, kGTargetItems, target_k, kQTargetItems};
+  int rc = timed(c, KIND_TAIL, [&] { launch_tail_lists(a, k0 & 1, pl.gc, n_units, tp, c->stream); });
+  if (rc != SN_OK) return rc;
+
+  GramArgs g = gram_args(c);
+  g.list = c->w.list_g;
+  g.ctl = c->w.ctl;
+  g.n_items = pl.g_items;  // grid: at most max(listed units, target) items
+  const int dh = c->shape.head_dim;
+  rc = timed(c, KIND_GRAM, [&] { launch_gram(c->shape.dtype == SN_BF16, dh, g.n_items, c->stream, g); });
+  if (rc != SN_OK) return rc;
+
+  IterArgs it = iter_args(c, a);
+  it.k0 = k0;
+  it.list = c->w.list_g;
+  it.ctl = c->w.ctl;
+  it.kvpos = c->w.kvpos;
   rc = timed(c, KIND_ITER, [&] { launch_gram_iterate(dh, pl.H, c->stream, it); });
   if (rc != SN_OK) return rc;
 
+  SweepArgs e = a;
+  e.k = 0;
+  e.only = c->w.alive + (size_t)(k0 & 1) * pl.H;  // the heads running after step k0
+  e.w.zn = c->w.zt;
+  TailLaunch tk{c->w.list_k, c->w.ctl + TC_EK, std::max(n_units, target_k)};
+  if ((rc = run_sweep(c, PH_EK, e, tk)) != SN_OK) return rc;
+  if (u) {
+    TailLaunch tq{c->w.list_g, c->w.ctl + TC_EQ, std::max(pl.H, kQTargetItems)};
+    if ((rc = run_sweep(c, PH_EQ, e, tq)) != SN_OK) return rc;
+  }
+  return SN_OK;
+}
+
+// The sweeps of the default form: first W_K sweep, then n_iter x (W_Q sweep,
+// W_K sweep).  In tolerance mode every W_K sweep decides, per head, whether
+// the step's sigma meets the rule; a stopped head's waves leave at set-up in
+// the later sweeps.  With d_h >= 16 only the first kTailSteps steps run as
+// full sweeps and the tail finishes the rest (run_tail).  Nothing waits on
+// the host.
+int run_chain(sn_ctx* c, SweepArgs a, float* u) {
+  const Plan& pl = c->plan;
+  int rc;
+  a.k = 0;
+  if ((rc = run_sweep(c, PH_INIT, a)) != SN_OK) return rc;
+  const int k_full = pl.tail ? std::min(a.n_iter, kTailSteps) : a.n_iter;
+  for (int k = 1; k <= k_full; ++k) {
+    a.k = k;
+    a.want_vec = (u != nullptr) && (c->params.tol > 0.f || k == a.n_iter);
+    if ((rc = run_sweep(c, PH_Q, a)) != SN_OK) return rc;
+    a.want_vec = 0;
+    if ((rc = run_sweep(c, PH_K, a)) != SN_OK) return rc;
+  }
+  if (pl.tail && a.n_iter > k_full) return run_tail(c, a, u, k_full);
+  return SN_OK;
+}
+
+// The Gram form of one call: first W_K sweep, Gram sweep, d_h-space
+// iteration, final W_K sweep (and W_Q sweep for u).
+int run_gram(sn_ctx* c, SweepArgs a, float* u) {
+  const Plan& pl = c->plan;
+  int rc;
+  a.k = 0;
+  if ((rc = run_sweep(c, PH_INIT, a)) != SN_OK) return rc;
+  GramArgs g = gram_args(c);
+  const int dh = c->shape.head_dim;
+  rc = timed(c, KIND_GRAM, [&] { launch_gram(c->shape.dtype == SN_BF16, dh, g.n_items, c->stream, g); });
+  if (rc != SN_OK) return rc;
+  IterArgs it = iter_args(c, a);
+  rc = timed(c, KIND_ITER, [&] { launch_gram_iterate(dh, pl.H, c->stream, it); });
+  if (rc != SN_OK) return rc;
   a.k = 0;  // the final sweeps write their ||v'||^2 partials to slot 0
   if ((rc = run_sweep(c, PH_EK, a)) != SN_OK) return rc;
   if (u && (rc = run_sweep(c, PH_EQ, a)) != SN_OK) return rc;
   return SN_OK;
+}
+
+// Views of the workspace of a plan.
+void bind_workspace(sn_ctx* c) {
+  const Plan& pl = c->plan;
+  char* ws = c->ws;
+  c->w = Work{};
+  c->w.zp = reinterpret_cast<float*>(ws + pl.off_zp);
+  c->w.zn = reinterpret_cast<float*>(ws + pl.off_zn);
+  c->w.yp = reinterpret_cast<float*>(ws + pl.off_yp);
+  c->w.yn = reinterpret_cast<float*>(ws + pl.off_yn);
+  c->w.sig = reinterpret_cast<float*>(ws + pl.off_sig);
+  c->w.vnorm0 = reinterpret_cast<float*>(ws + pl.off_vn);
+  c->w.alive = reinterpret_cast<int32_t*>(ws + pl.off_alive);
+  c->w.iters = reinterpret_cast<int32_t*>(ws + pl.off_iters);
+  if (pl.gram || pl.tail) c->w.fin = reinterpret_cast<float*>(ws + pl.off_fin);
+  if (pl.tail) {
+    c->w.zs = reinterpret_cast<int32_t*>(ws + pl.off_zs);
+    c->w.list_g = reinterpret_cast<int32_t*>(ws + pl.off_lg);
+    c->w.list_k = reinterpret_cast<int32_t*>(ws + pl.off_lk);
+    c->w.kvpos = reinterpret_cast<int32_t*>(ws + pl.off_kvpos);
+    c->w.ctl = reinterpret_cast<int32_t*>(ws + pl.off_ctl);
+    c->w.zt = reinterpret_cast<float*>(ws + pl.off_zt);
+  }
+}
+
+// One spectral_step call on a bound context (table already in place).
+int step_body(sn_ctx* c, float* v, float* u, int32_t n_iter, float* sigma, float* scale, int32_t* iters) {
+  const Plan& pl = c->plan;
+  const int L = c->shape.n_layers;
+  SweepArgs a{};
+  a.ld = c->shape.ld;
+  a.d = c->shape.d_model;
+  a.n_q = c->shape.n_q_heads;
+  a.n_kv = c->shape.n_kv_heads;
+  a.g = pl.g;
+  a.H = pl.H;
+  a.s_q = pl.s_q;
+  a.s_k = pl.s_k;
+  a.n_tiles = pl.n_tiles;
+  a.nch = pl.nch;
+  a.n_iter = n_iter;
+  a.tol = c->params.tol;
+  a.w = c->w;
+  a.v = v;
+  a.u = u;
+  a.sigma = sigma;
+  a.iters = iters ? iters : c->w.iters;
+
+  int rc = pl.gram ? run_gram(c, a, u) : run_chain(c, a, u);
+  if (rc != SN_OK) return rc;
+
+  const bool tail_ran = pl.tail && n_iter > kTailSteps;
+  FinArgs f{};
+  f.H = pl.H;
+  f.L = L;
+  f.n_q = c->shape.n_q_heads;
+  f.d = c->shape.d_model;
+  f.s_k = pl.s_k;
+  f.slot_fixed = pl.gram ? 0 : -1;
+  f.zs = pl.tail ? c->w.zs : nullptr;
+  f.tail = tail_ran ? c->w.alive + (size_t)(kTailSteps & 1) * pl.H : nullptr;
+  f.zt = c->w.zt;
+  f.coef = scale_coef(c);
+  f.w = c->w;
+  f.v = v;
+  f.u = u;
+  f.sigma = sigma;
+  f.scale = scale;
+  f.iters = a.iters;
+  return timed(c, KIND_FIN, [&] { launch_finalize(pl.H + L, c->stream, f); });
 }
 
 }  // namespace
@@ -532,27 +674,12 @@ SN_API int spectral_init(sn_ctx** ctx, const sn_shape* shape, const sn_params* p
   if (hipGetDevice(&c->device) != hipSuccess) return cleanup(fail(SN_ESTATE, "no HIP device"));
   const size_t L = c->shape.n_layers;
   if (hipMalloc(&c->ws, c->plan.bytes) != hipSuccess) return cleanup(fail(SN_EHIP, "hipMalloc(workspace) failed"));
-  if (hipMalloc(&c->d_tab, 2 * L * sizeof(void*)) != hipSuccess)
+  if (hipMalloc(&c->d_tab, 4 * L * sizeof(void*)) != hipSuccess)
     return cleanup(fail(SN_EHIP, "hipMalloc(pointer table) failed"));
-  if (hipHostMalloc(&c->h_tab, 2 * L * sizeof(void*), hipHostMallocDefault) != hipSuccess)
-    return cleanup(fail(SN_EHIP, "hipHostMalloc(pointer table) failed"));
-  if (hipHostMalloc(&c->h_alive, 2 * sizeof(int32_t), hipHostMallocDefault) != hipSuccess)
-    return cleanup(fail(SN_EHIP, "hipHostMalloc failed"));
   if (hipEventCreateWithFlags(&c->tab_event, hipEventDisableTiming) != hipSuccess)
     return cleanup(fail(SN_EHIP, "hipEventCreate failed"));
-  const Plan& pl = c->plan;
-  c->w.zp = reinterpret_cast<float*>(c->ws + pl.off_zp);
-  c->w.zn = reinterpret_cast<float*>(c->ws + pl.off_zn);
-  c->w.yp = reinterpret_cast<float*>(c->ws + pl.off_yp);
-  c->w.yn = reinterpret_cast<float*>(c->ws + pl.off_yn);
-  c->w.sig = reinterpret_cast<float*>(c->ws + pl.off_sig);
-  c->w.vnorm0 = reinterpret_cast<float*>(c->ws + pl.off_vn);
-  c->w.alive = reinterpret_cast<int32_t*>(c->ws + pl.off_alive);
-  c->w.n_alive = reinterpret_cast<int32_t*>(c->ws + pl.off_nalive);
-  c->w.iters = reinterpret_cast<int32_t*>(c->ws + pl.off_iters);
-  c->w.fin = pl.gram ? reinterpret_cast<float*>(c->ws + pl.off_fin) : nullptr;
-  c->w.zs = pl.tail ? reinterpret_cast<int32_t*>(c->ws + pl.off_zs) : nullptr;
-  c->w.list = pl.tail ? reinterpret_cast<int32_t*>(c->ws + pl.off_list) : nullptr;
+  c->tab = c->d_tab;
+  bind_workspace(c);
   *ctx = c;
   return SN_OK;
 }
@@ -560,13 +687,14 @@ SN_API int spectral_init(sn_ctx** ctx, const sn_shape* shape, const sn_params* p
 SN_API int spectral_set_stream(sn_ctx* c, void* hip_stream) {
   if (!c) return fail(SN_ENULL, "ctx must not be NULL");
   hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
-  // later launches read the device pointer table, whose last copy was queued
-  // on the previous stream: order the new stream after it (a stream being
-  // captured into a graph cannot wait on an outside event; its launches run
-  // at replay, after the copy)
-  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
-  SN_HIP(hipStreamIsCapturing(st, &cap));
-  if (cap == hipStreamCaptureStatusNone && st != c->stream) SN_HIP(hipStreamWaitEvent(st, c->tab_event, 0));
+  // later launches share the workspace and the eager pointer table with the
+  // work queued on the previous stream: order the new stream after all of it
+  // (a stream being captured into a graph cannot wait on an outside event;
+  // its launches run at replay)
+  if (st != c->stream && !capturing(st) && !capturing(c->stream)) {
+    SN_HIP(hipEventRecord(c->tab_event, c->stream));
+    SN_HIP(hipStreamWaitEvent(st, c->tab_event, 0));
+  }
   c->stream = st;
   return SN_OK;
 }
@@ -580,10 +708,8 @@ SN_API void spectral_destroy(sn_ctx* c) {
   }
   for (auto e : c->pool) (void)hipEventDestroy(e);
   if (c->tab_event) (void)hipEventDestroy(c->tab_event);
-  if (c->h_alive) (void)hipHostFree(c->h_alive);
-  if (c->h_tab) (void)hipHostFree(c->h_tab);
-  if (c->d_tab) (void)hipFree(c->d_tab);
-  if (c->ws) (void)hipFree(c->ws);
+  if (c->owns_ws && c->d_tab) (void)hipFree(c->d_tab);
+  if (c->owns_ws && c->ws) (void)hipFree(c->ws);
   delete c;
 }
 
@@ -618,49 +744,9 @@ SN_API int spectral_step(sn_ctx* c, const void* const* wq_layers, const void* co
   if (!wq_layers || !wk_layers || !v || !sigma || !scale)
     return fail(SN_ENULL, "wq_layers, wk_layers, v, sigma and scale must not be NULL");
   if (n_iter < 1) return fail(SN_EINVAL, "n_iter must be >= 1");
-  const int L = c->shape.n_layers;
-  int rc = update_table(c, wq_layers, wk_layers);
+  const int rc = update_table(c, wq_layers, wk_layers);
   if (rc != SN_OK) return rc;
-
-  const Plan& pl = c->plan;
-  SweepArgs a{};
-  a.ld = c->shape.ld;
-  a.d = c->shape.d_model;
-  a.n_q = c->shape.n_q_heads;
-  a.n_kv = c->shape.n_kv_heads;
-  a.g = pl.g;
-  a.H = pl.H;
-  a.s_q = pl.s_q;
-  a.s_k = pl.s_k;
-  a.n_tiles = pl.n_tiles;
-  a.nch = pl.nch;
-  a.n_iter = n_iter;
-  a.tol = c->params.tol;
-  a.w = c->w;
-  a.v = v;
-  a.u = u;
-  a.sigma = sigma;
-  a.iters = iters ? iters : c->w.iters;
-
-  rc = pl.gram ? run_gram(c, a, u) : run_chain(c, a, u);
-  if (rc != SN_OK) return rc;
-
-  FinArgs f{};
-  f.H = pl.H;
-  f.L = L;
-  f.n_q = c->shape.n_q_heads;
-  f.d = c->shape.d_model;
-  f.s_k = pl.s_k;
-  f.slot_fixed = pl.gram ? 0 : -1;
-  f.zs = pl.tail ? c->w.zs : nullptr;
-  f.coef = scale_coef(c);
-  f.w = c->w;
-  f.v = v;
-  f.u = u;
-  f.sigma = sigma;
-  f.scale = scale;
-  f.iters = a.iters;
-  return timed(c, KIND_FIN, [&] { launch_finalize(pl.H + L, c->stream, f); });
+  return step_body(c, v, u, n_iter, sigma, scale, iters);
 }
 
 SN_API int spectral_step_layer(sn_ctx* c, const void* const* wq_layers, const void* const* wk_layers, float* v,
@@ -763,24 +849,23 @@ SN_API int spectral_logits_fp8(sn_ctx* c, const void* const* x_layers, int64_t l
   if (workspace_bytes < need) return fail(SN_EINVAL, "workspace too small (spectral_logits_workspace_bytes)");
   if ((reinterpret_cast<uintptr_t>(workspace) & 255) || (reinterpret_cast<uintptr_t>(codes) & 15))
     return fail(SN_EINVAL, "workspace must be 256-byte and codes 16-byte aligned");
-  std::vector<const void*> tab(3 * (size_t)L);
   for (int l = 0; l < L; ++l) {
     if (!x_layers[l] || !wq_layers[l] || !wk_layers[l]) return fail(SN_ENULL, "a layer pointer is NULL");
     if ((reinterpret_cast<uintptr_t>(x_layers[l]) | reinterpret_cast<uintptr_t>(wq_layers[l]) |
          reinterpret_cast<uintptr_t>(wk_layers[l])) & 15)
       return fail(SN_EINVAL, "layer pointers must be 16-byte aligned");
-    tab[l] = x_layers[l];
-    tab[L + l] = wq_layers[l];
-    tab[2 * L + l] = wk_layers[l];
   }
   int cur_dev = 0;
   SN_HIP(hipGetDevice(&cur_dev));
   if (cur_dev != c->device) return fail(SN_ESTATE, "the current HIP device is not the context's device");
 
-  // pointer tables at the start of the workspace (copied from pageable host
-  // memory: the runtime stages it before the call returns)
+  // pointer tables at the start of the workspace, written by a kernel whose
+  // arguments carry the pointers (so the call can be captured into a graph)
   const void** d_tab = reinterpret_cast<const void**>(workspace);
-  SN_HIP(hipMemcpyAsync(d_tab, tab.data(), tab.size() * sizeof(void*), hipMemcpyHostToDevice, c->stream));
+  int rc = fill_table(d_tab, 3 * L,
+                      [&](int i) { return i < L ? x_layers[i] : i < 2 * L ? wq_layers[i - L] : wk_layers[i - 2 * L]; },
+                      c->stream);
+  if (rc != SN_OK) return rc;
   uint16_t* planes = reinterpret_cast<uint16_t*>(reinterpret_cast<char*>(workspace) + ((3 * L * 8 + 255) & ~255));
   const size_t qn = (size_t)L * seq_len * nq_cols, kn = (size_t)L * seq_len * nk_cols;
   ProjArgs p{};
@@ -814,7 +899,7 @@ SN_API int spectral_logits_fp8(sn_ctx* c, const void* const* x_layers, int64_t l
   g.codes = codes;
   g.max_abs = max_abs;
   g.n_over = n_over;
-  int rc = timed(c, KIND_LOGITS, [&] { sn_launch_zero_stats(max_abs, n_over, L * sh.n_q_heads, c->stream); });
+  rc = timed(c, KIND_LOGITS, [&] { sn_launch_zero_stats(max_abs, n_over, L * sh.n_q_heads, c->stream); });
   if (rc != SN_OK) return rc;
   if ((rc = timed(c, KIND_PROJ, [&] { sn_launch_proj(p, c->stream); })) != SN_OK) return rc;
   return timed(c, KIND_LOGITS, [&] { sn_launch_logits(g, dh, c->stream); });

@@ -19,9 +19,11 @@
 //     expansion): v'[c] = sum_r K[r,c] y_h[r], ||v'||^2, z_h[r] partials.
 //     With bf16 weights and 3..8 query heads per KV head, ksweep_mfma_kernel
 //     does this on the matrix cores from a tile staged once in LDS.
-// In tolerance mode, once few heads still run, the sweeps are launched over
-// lists of the running query heads and of the W_K units that hold one
-// (tail_lists_kernel), item r decoding to list entry r instead of r itself.
+// In tolerance mode the heads still running after the first steps are
+// finished in d_h-space (gram.hip); the final sweeps that map their last
+// vectors back to d-space are launched over lists of those heads and of the
+// W_K units holding one (tail_lists_kernel), item r decoding to list entry r
+// instead of r itself, with the count and strips read from the device.
 // Partials (one d_h vector and one squared norm per strip) go to a small
 // workspace and are summed, in a fixed order, by the consumer of the next
 // sweep, which also normalises (y /= sigma, z /= ||v'||).  Every reduction
@@ -58,11 +60,7 @@ __device__ __forceinline__ Item decode_item(const SweepArgs& a, int item) {
   bool valid_item = item < a.n_items;
   it.strip = valid_item ? item % a.s_out : 0;
   int rest = valid_item ? item / a.s_out : 0;
-  if (a.list && valid_item) {  // tail launch: only the listed heads / units
-    rest = uni(a.list[rest]);
-    valid_item = rest >= 0;
-    if (!valid_item) rest = 0;
-  }
+  if (a.list && valid_item) rest = uni(a.list[rest]);  // tail launch: only the listed heads / units
   if (PH == PH_Q || PH == PH_EQ) {  // one query head per item
     it.layer = rest / a.n_q;
     it.row0 = (rest % a.n_q) * DH;
@@ -117,7 +115,6 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
     }
   }
   // ---- per-head decisions (wave-uniform)
-  int n_cont = 0;
   float inv[GC];
   const float* part[GC];
 #pragma unroll
@@ -133,12 +130,13 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
       if (strip == 0 && lane == 0) a.w.alive[hh] = 1;  // slot 0
       continue;
     }
-    if (PH == PH_EK || PH == PH_EQ) {  // final sweeps of the Gram form: heads that ran
-      act[i] = uni(a.iters[hh]) > 0;
+    if (PH == PH_EK || PH == PH_EQ) {  // final sweeps of the Gram form / the tail: heads that ran
+      act[i] = uni(a.iters[hh]) > 0 && (!a.only || uni(a.only[hh]) != 0);
       last[i] = act[i];
       if (act[i]) {
         const float* src = a.w.fin + (size_t)hh * 2 * DH + (PH == PH_EK ? DH : 0);
         for (int r = lane; r < DH; r += 64) xs[i][r] = src[r];
+        if (PH == PH_EK && a.only && a.w.zs && strip == 0 && lane == 0) a.w.zs[hh] = a.s_out;
       }
       continue;
     }
@@ -194,11 +192,9 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
         }
         a.w.alive[slot_cur * a.H + hh] = (act[i] && !last[i]) ? 1 : 0;
       }
-      n_cont += (act[i] && !last[i]) ? 1 : 0;
     }
     if (PH == PH_Q && dead_v) act[i] = false;
   }
-  if (PH == PH_K && strip == 0 && lane == 0 && n_cont > 0) atomicAdd(&a.w.n_alive[slot_cur], n_cont);
   if (!ITER) return;
 
   // ---- normalised input vectors: partial t of every active head, t = 0, 1, ...
@@ -232,17 +228,30 @@ __device__ __forceinline__ void head_setup(const SweepArgs& a, const Item& itm, 
   }
 }
 
+// Final sweeps of the tolerance-mode tail: the count of listed entries and
+// the strips chosen for it come from the device control block.
+template <int PH>
+__device__ __forceinline__ void apply_tail_ctl(SweepArgs& a) {
+  if constexpr (PH == PH_EK || PH == PH_EQ) {
+    if (a.ctl) {
+      a.s_out = uni(a.ctl[1]);
+      a.tps = uni(a.ctl[2]);
+      a.n_items = uni(a.ctl[0]) * a.s_out;
+    }
+  }
+}
+
 template <typename T, int DH, int GC, int PH>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(waves_hint<DH, GC>())))
-sweep_kernel(SweepArgs a) {
+sweep_kernel(SweepArgs args) {
+  SweepArgs a = args;
+  apply_tail_ctl<PH>(a);
   constexpr int VEC = Traits<T>::VEC;
   constexpr int CPL = kCPL;  // 16-byte column chunks per wave row: 128-byte row segments
   constexpr int RPL = DH / kRG;
   constexpr int TILE_C = CPL * VEC;
   static_assert(DH % kRG == 0, "head_dim must be a multiple of 8");
   __shared__ float xs[kWaves][GC][DH];
-
-  if (PH == PH_Q && blockIdx.x == 0 && threadIdx.x == 0) a.w.n_alive[a.k & 1] = 0;
 
   const int lane = threadIdx.x & 63;
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
@@ -473,7 +482,9 @@ __device__ __forceinline__ bool pick(const bool (&f)[GC], int i) {
 
 template <int DH, int PH>
 __global__ void __launch_bounds__(64 * kMWaves) __attribute__((amdgpu_waves_per_eu(2)))
-ksweep_mfma_kernel(SweepArgs a) {
+ksweep_mfma_kernel(SweepArgs args) {
+  SweepArgs a = args;
+  apply_tail_ctl<PH>(a);
   constexpr int GC = 8;
   constexpr int RB = DH / 16;          // 16-row blocks (product-2 M blocks)
   constexpr int KB = DH / 32;          // 32-row blocks (product-1 K blocks)
@@ -711,9 +722,13 @@ __global__ void __launch_bounds__(kThreads) finalize_kernel(FinArgs f) {
     bool touch_v = false;
     if (it > 0) {
       float n2 = 0.f;
-      const int slot = f.slot_fixed >= 0 ? f.slot_fixed : (it & 1);
       const int sk = f.zs ? f.zs[b] : f.s_k;
-      for (int s = 0; s < sk; ++s) n2 += f.w.zn[((size_t)slot * f.H + b) * sk + s];
+      if (f.tail && f.tail[b] != 0) {  // finished by the tail: the final W_K sweep's own buffer
+        for (int s = 0; s < sk; ++s) n2 += f.zt[(size_t)b * sk + s];
+      } else {
+        const int slot = f.slot_fixed >= 0 ? f.slot_fixed : (it & 1);
+        for (int s = 0; s < sk; ++s) n2 += f.w.zn[((size_t)slot * f.H + b) * sk + s];
+      }
       vs = 1.0f / sqrtf(n2);
       us = 1.0f / f.sigma[b];
       touch_v = true;
@@ -749,13 +764,12 @@ __global__ void __launch_bounds__(kThreads) finalize_kernel(FinArgs f) {
   }
 }
 
-// Lists of the tolerance-mode tail, built by one workgroup after the W_K
-// sweep of parity `slot`: thread t owns a contiguous range of heads (then of
-// W_K units) and counts the running ones, and an exclusive scan of the counts
-// in LDS gives each thread its first place in the list, so both lists come
-// out in ascending order.  Entries past the last running one are -1 (up to
-// H, and up to n_units).  A head that stopped has its flag of the other
-// parity cleared too: it is not visited again, so no later sweep would.
+// Lists of the tolerance-mode tail, built by one workgroup from the running
+// flags after step k of the chain: thread t owns a contiguous range of
+// entries and counts the running ones, and an exclusive scan of the counts in
+// LDS gives each thread its first place in the list, so every list comes out
+// in ascending order.  Thread 0 then writes the counts, and the strips of
+// each compacted launch for its count, to the control block (TC_*).
 constexpr int kTailThreads = 1024;
 
 __device__ __forceinline__ int block_exclusive_scan(int x, int* buf, int* total) {
@@ -774,30 +788,61 @@ __device__ __forceinline__ int block_exclusive_scan(int x, int* buf, int* total)
   return incl - x;
 }
 
+// Strips for a compacted launch over `count` entries: about target / count
+// (rounded down, so count * strips <= max(count, target)), at least
+// kTailMinTiles tiles each.
+__device__ __forceinline__ void tail_strips(int count, int n_tiles, int target, int32_t* out) {
+  int s = count > 0 ? max(1, target / count) : 1;
+  s = max(1, min(s, max(1, n_tiles / kTailMinTiles)));
+  const int tps = (n_tiles + s - 1) / s;
+  out[0] = count;
+  out[1] = (n_tiles + tps - 1) / tps;
+  out[2] = tps;
+}
+
 __global__ void __launch_bounds__(kTailThreads)
-tail_lists_kernel(SweepArgs a, int slot, int gc, int n_units, int32_t* list_q, int32_t* list_k) {
+tail_lists_kernel(SweepArgs a, int slot, int gc, int n_units, TailPlan tp) {
   __shared__ int buf[kTailThreads];
   const int t = threadIdx.x;
   const int32_t* cur = a.w.alive + (size_t)slot * a.H;
-  int32_t* other = a.w.alive + (size_t)(slot ^ 1) * a.H;
-  int total = 0;
+  int32_t* list_g = a.w.list_g;
 
+  // running query heads: list_g[0 .. nq)
+  int nq = 0;
   const int per_h = (a.H + kTailThreads - 1) / kTailThreads;
   const int h0 = min(a.H, t * per_h), h1 = min(a.H, h0 + per_h);
   int n = 0;
   for (int hh = h0; hh < h1; ++hh) n += cur[hh] != 0 ? 1 : 0;
-  int pos = block_exclusive_scan(n, buf, &total);
-  for (int hh = h0; hh < h1; ++hh) {
-    if (cur[hh] != 0)
-      list_q[pos++] = hh;
-    else
-      other[hh] = 0;
-  }
-  for (int i = total + t; i < a.H; i += kTailThreads) list_q[i] = -1;
+  int pos = block_exclusive_scan(n, buf, &nq);
+  for (int hh = h0; hh < h1; ++hh)
+    if (cur[hh] != 0) list_g[pos++] = hh;
 
-  // unit u = (layer * n_kv + j) * nch + ch holds query heads
+  // key heads x = layer * n_kv + j serving a running head: list_g[nq ..) = H + x
+  const int n_kvh = (a.H / a.n_q) * a.n_kv;
+  auto kv_running = [&](int x) {
+    const int head0 = (x / a.n_kv) * a.n_q + (x % a.n_kv) * a.g;
+    bool r = false;
+    for (int i = 0; i < a.g; ++i) r = r || cur[head0 + i] != 0;
+    return r;
+  };
+  int nk = 0;
+  const int per_x = (n_kvh + kTailThreads - 1) / kTailThreads;
+  const int x0 = min(n_kvh, t * per_x), x1 = min(n_kvh, x0 + per_x);
+  int m = 0;
+  for (int x = x0; x < x1; ++x) m += kv_running(x) ? 1 : 0;
+  pos = block_exclusive_scan(m, buf, &nk);
+  for (int x = x0; x < x1; ++x) {
+    if (kv_running(x)) {
+      a.w.kvpos[x] = pos;
+      list_g[nq + pos++] = a.H + x;
+    } else {
+      a.w.kvpos[x] = -1;
+    }
+  }
+
+  // W_K units u = (layer * n_kv + j) * nch + ch holding a running head: query heads
   // layer * n_q + j * g + ch * gc + (0 .. min(gc, g - ch * gc) - 1)
-  auto running = [&](int un) {
+  auto unit_running = [&](int un) {
     const int grp = un / a.nch, ch = un % a.nch;
     const int head0 = (grp / a.n_kv) * a.n_q + (grp % a.n_kv) * a.g + ch * gc;
     const int nv = min(gc, a.g - ch * gc);
@@ -805,14 +850,22 @@ tail_lists_kernel(SweepArgs a, int slot, int gc, int n_units, int32_t* list_q, i
     for (int i = 0; i < nv; ++i) r = r || cur[head0 + i] != 0;
     return r;
   };
+  int nu = 0;
   const int per_u = (n_units + kTailThreads - 1) / kTailThreads;
   const int u0 = min(n_units, t * per_u), u1 = min(n_units, u0 + per_u);
-  int m = 0;
-  for (int un = u0; un < u1; ++un) m += running(un) ? 1 : 0;
-  pos = block_exclusive_scan(m, buf, &total);
+  m = 0;
+  for (int un = u0; un < u1; ++un) m += unit_running(un) ? 1 : 0;
+  pos = block_exclusive_scan(m, buf, &nu);
   for (int un = u0; un < u1; ++un)
-    if (running(un)) list_k[pos++] = un;
-  for (int i = total + t; i < n_units; i += kTailThreads) list_k[i] = -1;
+    if (unit_running(un)) a.w.list_k[pos++] = un;
+
+  if (t == 0) {
+    int32_t* c = a.w.ctl;
+    tail_strips(nq + nk, tp.n_tiles_g, tp.target_g, c + TC_GRAM);
+    tail_strips(nu, tp.n_tiles_k, tp.target_k, c + TC_EK);
+    tail_strips(nq, tp.n_tiles_q, tp.target_q, c + TC_EQ);
+    c[TC_NQ] = nq;
+  }
 }
 
 template <typename T, int DH, int GC>
@@ -881,9 +934,8 @@ void launch_finalize(int blocks, hipStream_t st, const FinArgs& f) {
   finalize_kernel<<<dim3(blocks), kThreads, 0, st>>>(f);
 }
 
-void launch_tail_lists(const SweepArgs& a, int slot, int gc, int n_units, int32_t* list_q, int32_t* list_k,
-                       hipStream_t st) {
-  tail_lists_kernel<<<dim3(1), kTailThreads, 0, st>>>(a, slot, gc, n_units, list_q, list_k);
+void launch_tail_lists(const SweepArgs& a, int slot, int gc, int n_units, const TailPlan& tp, hipStream_t st) {
+  tail_lists_kernel<<<dim3(1), kTailThreads, 0, st>>>(a, slot, gc, n_units, tp);
 }
 
 }  // namespace sn

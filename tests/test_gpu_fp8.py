@@ -148,6 +148,34 @@ def test_zero_tokens_give_zero_logits():
     est.close()
 
 
+def test_non_finite_scale_counts_every_logit_as_overflow():
+    """A NaN scale (a layer with a degenerate head) and a zero scale: every
+    scaled logit is non-finite, so every one counts as an overflow, every
+    code is the NaN code, and max |S~| is not finite (NaN for the NaN scale),
+    as the oracle's statistics say."""
+    wl = WORKLOADS["llama2-70b-gqa"].replace(key="nan-scale", std=0.02, n_layers=2, d_model=256, n_q=4, n_kv=2,
+                                              head_dim=64)
+    seq = 70
+    wq, wk = all_weights(wl, "cpu")
+    xs = [layer_tokens(wl, seq, l) for l in range(wl.n_layers)]
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha)
+    scales = [float("nan"), 0.0]
+    max_abs, n_over, codes = est.logits_fp8(torch.stack(xs).cuda(), wq.cuda(), wk.cuda(),
+                                            torch.tensor(scales, device="cuda"), want_codes=True)
+    torch.cuda.synchronize()
+    max_abs, n_over, codes = max_abs.cpu().numpy(), n_over.cpu().numpy(), codes.cpu().numpy()
+    assert (n_over == seq * seq).all(), n_over
+    assert np.isnan(max_abs[0]).all() and not np.isfinite(max_abs[1]).any()
+    assert ((codes & 0x7F) == e4m3.NAN_CODE).all()
+    with np.errstate(divide="ignore", invalid="ignore"):
+        for l in range(wl.n_layers):
+            ref = fp8_consumer.consume_layer(xs[l].double().numpy(), wq[l].double().numpy(), wk[l].double().numpy(),
+                                             scales[l], wl.n_kv, wl.head_dim, want_codes=False)
+            assert [ref["n_over"][h] for h in range(wl.n_q)] == list(n_over[l])
+            assert all(not np.isfinite(ref["max_abs"][h]) for h in range(wl.n_q))
+    est.close()
+
+
 def test_full_size_70b_sampled_heads():
     """Llama-2-70B GQA shape, 1024 tokens per layer, all 80 layers on the GPU;
     two heads of two layers against the oracle.  Per-layer scales are seeded

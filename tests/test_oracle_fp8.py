@@ -86,3 +86,22 @@ def test_rank_one_closed_form_counts():
     assert out["n_over"][0] == 4
     assert out["max_abs"][0] == pytest.approx(495.0)
     assert np.count_nonzero((out["codes"][0] & 0x7F) == e4m3.NAN_CODE) == 4
+
+
+def test_non_finite_scaled_logits_count_as_overflows():
+    """Sec. 1: an overflow is a logit E4M3 cannot hold, which turns into NaN.
+    |x| > 448 is the paper's predicate; NaN and +-inf (e.g. logits scaled by a
+    NaN or zero scale) are not representable either, so they count, and their
+    codes are the NaN code.  A NaN scale makes every logit of the layer an
+    overflow and the largest scaled logit NaN."""
+    x = np.array([np.nan, np.inf, -np.inf, 448.0, -448.0, 448.0001, 0.0, -1e9])
+    np.testing.assert_array_equal(e4m3.overflows(x), [True, True, True, False, False, True, False, True])
+    assert ((e4m3.encode(x[:3]) & 0x7F) == e4m3.NAN_CODE).all()
+    wl = WORKLOADS["tiny"].replace(n_q=4, n_kv=2)
+    wq, wk = layer_weights(wl, 0)
+    xs = tokens(wl, 10, spherical=True)
+    r = fp8_consumer.consume_layer(xs, wq.double().numpy(), wk.double().numpy(), float("nan"), wl.n_kv,
+                                   wl.head_dim)
+    for h in range(wl.n_q):
+        assert r["n_over"][h] == 100 and math.isnan(r["max_abs"][h])
+        assert ((r["codes"][h] & 0x7F) == e4m3.NAN_CODE).all()

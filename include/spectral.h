@@ -162,6 +162,25 @@ SN_API int spectral_step(sn_ctx* ctx, const void* const* wq_layers, const void* 
                          float* v, float* u, int32_t n_iter, float* sigma, float* scale,
                          int32_t* iters);
 
+/* Allocation-free variant of spectral_step, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  It needs no context: shape, params
+ * (SN_FLAG_LAYER ignored) and hip_stream as for spectral_init, the other
+ * arguments as for spectral_step, whose results it gives bit for bit.  Its
+ * workspace and layer-pointer table live in a static device array of
+ * 32 MiB that each device holds from the first call on it until the process
+ * ends; a shape whose workspace (spectral_workspace_bytes) plus 4 n_layers
+ * pointers, rounded up to 256 bytes, does not fit is rejected with
+ * SN_EINVAL before anything is queued.  The call allocates nothing (no
+ * hipMalloc, hipFree, event or allocating library routine).  Every call on
+ * a device shares that device's array, which keeps the last call's
+ * contents: calls that overlap on one device (queued on different streams,
+ * or from several threads without ordering) race and give wrong results.
+ * Errors: SN_ENULL, SN_EINVAL, SN_EDTYPE, SN_ESTATE, SN_EHIP. */
+SN_API int spectral_step_noalloc(const sn_shape* shape, const sn_params* params, const void* const* wq_layers,
+                                 const void* const* wk_layers, float* v, float* u, int32_t n_iter, float* sigma,
+                                 float* scale, int32_t* iters, void* hip_stream);
+
 /* The layer-level estimator exactly as the paper prints it (App. E,
  * "Implicit GQA Power Iteration"; g = 1 is the multi-head algorithm of
  * Sec. 4.1): one pair u, v in R^d per layer for the concatenated

@@ -18,6 +18,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -264,6 +265,7 @@ struct sn_ctx {
   Work w{};
   const void** d_tab = nullptr;  // device [2][2L]: the eager table, then the table of captured calls
   const void** tab = nullptr;    // the table the current call's launches read
+  bool cache_table = true;       // eager calls skip the table write when the pointers did not change
   std::vector<const void*> cached;  // pointers in the eager table
   hipEvent_t tab_event = nullptr;
   bool prof = false;
@@ -374,6 +376,7 @@ int update_table(sn_ctx* c, const void* const* wq_layers, const void* const* wk_
     return fill_table(c->tab, 2 * L, src, c->stream);
   }
   c->tab = c->d_tab;
+  if (!c->cache_table) return fill_table(c->tab, 2 * L, src, c->stream);
   bool same = c->cached.size() == (size_t)(2 * L);
   for (int l = 0; same && l < L; ++l)
     same = c->cached[l] == wq_layers[l] && c->cached[L + l] == wk_layers[l];
@@ -747,6 +750,81 @@ SN_API int spectral_step(sn_ctx* c, const void* const* wq_layers, const void* co
   const int rc = update_table(c, wq_layers, wk_layers);
   if (rc != SN_OK) return rc;
   return step_body(c, v, u, n_iter, sigma, scale, iters);
+}
+
+}  // extern "C"
+
+// ---- the allocation-free variant of spectral_step
+//
+// Its workspace and pointer table live in `scratch`, a static device array of
+// kScratchBytes that each device holds from the library's first use on it
+// until the process ends.  Host code reaches a device's copy only through the
+// address hipGetSymbolAddress returns on that device (the array's name in
+// host code is a host-side stand-in), kept per device here.  Nothing in the
+// workspace must start at zero: every buffer a kernel reads was written
+// earlier in the same call (the running flags by the first sweep, partials
+// by their producer sweep, the tail's lists and control block by its list
+// kernel).
+namespace {
+
+constexpr size_t kScratchBytes = size_t(32) << 20;
+constexpr int kMaxDevices = 64;
+
+static __device__ __attribute__((aligned(256))) uint8_t scratch[kScratchBytes];
+
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this device's scratch (the current device), looked up
+// once per device.
+int scratch_on_device(int dev, char** out) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(SN_ESTATE, "device ordinal beyond the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    SN_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(SN_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch_ptr[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return SN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+SN_API int spectral_step_noalloc(const sn_shape* shape, const sn_params* params, const void* const* wq_layers,
+                                 const void* const* wk_layers, float* v, float* u, int32_t n_iter, float* sigma,
+                                 float* scale, int32_t* iters, void* hip_stream) {
+  if (!wq_layers || !wk_layers || !v || !sigma || !scale)
+    return fail(SN_ENULL, "wq_layers, wk_layers, v, sigma and scale must not be NULL");
+  int rc = validate(shape, params);
+  if (rc != SN_OK) return rc;
+  if (n_iter < 1) return fail(SN_EINVAL, "n_iter must be >= 1");
+  sn_ctx c;
+  c.shape = *shape;
+  if (c.shape.ld == 0) c.shape.ld = shape->d_model;
+  c.params = *params;
+  c.params.flags &= ~SN_FLAG_LAYER;  // only reserves space for spectral_step_layer
+  c.plan = make_plan(&c.shape, &c.params);
+  const int L = c.shape.n_layers;
+  const size_t tab_bytes = ((size_t)4 * L * sizeof(void*) + 255) & ~size_t(255);
+  const size_t need = tab_bytes + c.plan.bytes;
+  if (need > kScratchBytes)
+    return fail(SN_EINVAL, "this shape needs " + std::to_string(need) + " bytes of scratch; spectral_step_noalloc " +
+                               "holds at most " + std::to_string(kScratchBytes) + " (use spectral_init / spectral_step)");
+  SN_HIP(hipGetDevice(&c.device));
+  char* base = nullptr;
+  if ((rc = scratch_on_device(c.device, &base)) != SN_OK) return rc;
+  c.stream = reinterpret_cast<hipStream_t>(hip_stream);
+  c.owns_ws = false;
+  c.cache_table = false;
+  c.d_tab = reinterpret_cast<const void**>(base);
+  c.ws = base + tab_bytes;
+  bind_workspace(&c);
+  if ((rc = update_table(&c, wq_layers, wk_layers)) != SN_OK) return rc;
+  return step_body(&c, v, u, n_iter, sigma, scale, iters);
 }
 
 SN_API int spectral_step_layer(sn_ctx* c, const void* const* wq_layers, const void* const* wk_layers, float* v,

@@ -28,6 +28,7 @@ SN_PROFILE_KINDS = len(KIND_NAMES)
 EXPORTED = (
     "spectral_init",
     "spectral_step",
+    "spectral_step_noalloc",
     "spectral_step_layer",
     "spectral_set_stream",
     "spectral_destroy",
@@ -90,6 +91,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.spectral_init.restype = ctypes.c_int
     lib.spectral_step.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp, i32, vp, vp, vp]
     lib.spectral_step.restype = ctypes.c_int
+    lib.spectral_step_noalloc.argtypes = [ctypes.POINTER(sn_shape), ctypes.POINTER(sn_params), ctypes.POINTER(vp),
+                                          ctypes.POINTER(vp), vp, vp, i32, vp, vp, vp, vp]
+    lib.spectral_step_noalloc.restype = ctypes.c_int
     lib.spectral_step_layer.argtypes = [vp, ctypes.POINTER(vp), ctypes.POINTER(vp), vp, vp, i32, vp, vp]
     lib.spectral_step_layer.restype = ctypes.c_int
     lib.spectral_set_stream.argtypes = [vp, vp]
@@ -156,6 +160,17 @@ def spectral_step(ctx: int, wq_ptrs: Sequence[int], wk_ptrs: Sequence[int], v: i
     _check(load_library().spectral_step(ctypes.c_void_p(ctx), wq, wk, ctypes.c_void_p(v),
                                         ctypes.c_void_p(u or None), int(n_iter), ctypes.c_void_p(sigma),
                                         ctypes.c_void_p(scale), ctypes.c_void_p(iters or None)))
+
+
+def spectral_step_noalloc(shape: sn_shape, params: sn_params, wq_ptrs: Sequence[int], wk_ptrs: Sequence[int], v: int,
+                          u: int, n_iter: int, sigma: int, scale: int, iters: int, stream: int = 0) -> None:
+    n = len(wq_ptrs)
+    wq = (ctypes.c_void_p * n)(*wq_ptrs)
+    wk = (ctypes.c_void_p * n)(*wk_ptrs)
+    _check(load_library().spectral_step_noalloc(ctypes.byref(shape), ctypes.byref(params), wq, wk, ctypes.c_void_p(v),
+                                                ctypes.c_void_p(u or None), int(n_iter), ctypes.c_void_p(sigma),
+                                                ctypes.c_void_p(scale), ctypes.c_void_p(iters or None),
+                                                ctypes.c_void_p(stream)))
 
 
 def spectral_step_layer(ctx: int, wq_ptrs: Sequence[int], wk_ptrs: Sequence[int], v: int, u: int, n_iter: int,

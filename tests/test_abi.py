@@ -128,3 +128,20 @@ def test_logit_consumer_workspace_holds_every_layer(lib):
         assert got == table + L * seq * (8 + 2) * 64 * 4
     with pytest.raises(sp.SpectralError):
         sp.spectral_logits_workspace_bytes(_shape(), 0)
+
+
+def test_noalloc_refuses_bad_calls_before_touching_the_device(lib):
+    """The allocation-free entry point checks its arguments and the size of
+    the workspace against its static scratch on the host, before any HIP call:
+    the 70B GQA shape in tolerance mode (240 MB of workspace) does not fit."""
+    one = [16] * 80
+    shape = _shape(n_layers=80, d_model=8192, n_q_heads=64, n_kv_heads=8, head_dim=128)
+    with pytest.raises(sp.SpectralError) as e:
+        sp.spectral_step_noalloc(shape, _params(tol=1e-4), one, one, 16, 0, 3, 16, 16, 0)
+    assert e.value.code == sp.SN_EINVAL and "scratch" in sp.spectral_last_error()
+    with pytest.raises(sp.SpectralError) as e:
+        sp.spectral_step_noalloc(_shape(), _params(), [16, 16], [16, 16], 0, 0, 3, 16, 16, 0)
+    assert e.value.code == sp.SN_ENULL
+    with pytest.raises(sp.SpectralError) as e:
+        sp.spectral_step_noalloc(_shape(n_kv_heads=3), _params(), [16, 16], [16, 16], 16, 0, 3, 16, 16, 0)
+    assert e.value.code == sp.SN_EINVAL

@@ -160,17 +160,18 @@ def test_layer_form_without_flag_is_refused():
     est.close()
 
 
-def test_layer_form_full_size_sampled():
-    """Llama-2-70B GQA shape, all 80 layers on the GPU, two layers against the oracle."""
-    wl = WORKLOADS["llama2-70b-gqa"].replace(n_iter=12)
+def test_layer_form_full_size_every_layer():
+    """Llama-2-70B GQA shape, all 80 layers at the bench's 30 iterations, every
+    layer's sigma and scale against the oracle's layer-level estimator (each
+    layer's weights widened to float64 on the device, then copied back)."""
+    wl = WORKLOADS["llama2-70b-gqa"]
     gq, gk = all_weights(wl, "cuda")
     v0 = layer_start_vectors(wl)
     gpu = run_layer(wl, gq, gk, v0, wl.n_iter, want_u=False)
     assert np.isfinite(gpu["sigma"]).all()
-    layers = [0, wl.n_layers - 1]
     ref = {}
-    for l in layers:
-        wq_l, wk_l = gq[l].float().cpu().numpy(), gk[l].float().cpu().numpy()
+    for l in range(wl.n_layers):
+        wq_l, wk_l = gq[l].double().cpu().numpy(), gk[l].double().cpu().numpy()
         ref[l] = power_iteration_layer(wq_l.T, wk_l.T, v0[l].double().numpy(), wl.n_iter, wl.n_q // wl.n_kv,
                                        wl.head_dim)
     check(wl, gpu, ref)

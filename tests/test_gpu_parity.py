@@ -331,61 +331,105 @@ def _sampled_heads(wl, rng, full_layers, per_layer):
     return sorted(heads)
 
 
-def _check_sampled(wl, gq, gk, v0, n_iter, gpu, heads, tol=0.0):
-    cache = {}
-
-    def layer(l):
-        if l not in cache:
-            cache[l] = (gq[l].float().cpu().numpy(), gk[l].float().cpu().numpy())
-        return cache[l]
-
-    sig = {}
-    worst = 0.0
-    for (l, h) in heads:
-        wq_l, wk_l = layer(l)
-        WQ, WK = head_slices(wq_l, wk_l, h, wl.n_kv, wl.head_dim)
-        r = power_iteration(WQ, WK, v0[l, h].double().cpu().numpy(), n_iter, tol)
-        sig[(l, h)] = r.sigma
-        err = _rel(gpu["sigma"][l, h], r.sigma)
-        worst = max(worst, float(err))
-        assert err <= RTOL, (l, h, gpu["sigma"][l, h], r.sigma)
-        if tol == 0.0:
-            assert gpu["iters"][l, h] == r.iters
-        else:
-            assert abs(int(gpu["iters"][l, h]) - r.iters) <= 1
-        if len(cache) > 4:
-            cache.pop(next(iter(cache)))
-    for l in {l for (l, _) in heads}:
-        if all((l, h) in sig for h in range(wl.n_q)):
-            ref = layer_scale(max(sig[(l, h)] for h in range(wl.n_q)), wl.alpha, wl.d_model, wl.head_dim)
-            assert _rel(gpu["scale"][l], ref) <= RTOL
-    print(f"{wl.key}: {len(heads)} sampled heads, max rel err sigma {worst:.3e}")
-
-
 def _run_full(wl, gq, gk, v0, n_iter, tol=0.0, flags=0):
     est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha, tol=tol, flags=flags)
     v = v0.clone()
     sigma, scale, iters = est.step(gq, gk, v, n_iter)
     torch.cuda.synchronize()
     out = {"sigma": sigma.cpu().double().numpy(), "scale": scale.cpu().double().numpy(),
-           "iters": iters.cpu().numpy(), "v": v}
+           "iters": iters.cpu().numpy(), "v": v.cpu().numpy()}
     est.close()
     return out
 
 
-@pytest.mark.parametrize("form", FORMS)
+def _explicit_sample(wl, rng, every, edges):
+    """All heads of the first and last layer (with edges), then one seeded
+    head in every every-th layer."""
+    heads = [(l, h) for l in (0, wl.n_layers - 1) for h in range(wl.n_q)] if edges else []
+    for l in range(0, wl.n_layers, every):
+        heads.append((l, int(rng.integers(wl.n_q))))
+    return sorted(set(heads))
+
+
 @pytest.mark.parametrize("key", ["gpt2-xl", "llama2-7b-spiked", "llama2-70b-gqa"])
-def test_full_size_sampled(key, form):
+def test_full_size_every_head(key):
+    """Full-size workloads, both forms: every sigma_h and every per-layer
+    scale against the float64 oracle's spectral_step (implicit per-head
+    chain; its own max over the layer's heads and Eq. "scale"), one layer at
+    a time on the very weight bits and start vectors the GPU consumed; the
+    iteration counts equal; every v within the informational cosine bar.
+    Then a seeded sample of heads against the explicit route (M = W^Q_h
+    W^{K T}_{g(h)} formed in float64, dense power iteration)."""
+    from oracle.explicit import dense_power_iteration, interaction_matrix
     wl = WORKLOADS[key]
     gq, gk = all_weights(wl, "cuda")
     v0 = start_vectors(wl, "cuda")
-    gpu = _run_full(wl, gq, gk, v0, wl.n_iter, flags=FORMS[form])
-    assert np.isfinite(gpu["sigma"]).all() and (gpu["iters"] == wl.n_iter).all()
+    gpu = {form: _run_full(wl, gq, gk, v0, wl.n_iter, flags=FORMS[form]) for form in FORMS}
+    for g in gpu.values():
+        assert np.isfinite(g["sigma"]).all() and (g["iters"] == wl.n_iter).all()
+    v0c = v0.double().cpu().numpy()
     rng = np.random.default_rng(wl.cfg_id)
-    heads = _sampled_heads(wl, rng, [0, wl.n_layers - 1], 2)
-    _check_sampled(wl, gq, gk, v0, wl.n_iter, gpu, heads)
+    every, edges = {"gpt2-xl": (1, True), "llama2-7b-spiked": (4, False), "llama2-70b-gqa": (10, False)}[key]
+    sample = _explicit_sample(wl, rng, every, edges)
+    worst = {form: [0.0, 0.0, 1.0] for form in FORMS}   # sigma err, scale err, min |cos v|
+    e_worst = 0.0
+    for l in range(wl.n_layers):
+        wq_l, wk_l = gq[l].float().cpu().numpy(), gk[l].float().cpu().numpy()
+        ref = oracle_step([wq_l], [wk_l], v0c[l:l + 1], wl.n_iter, n_kv=wl.n_kv, head_dim=wl.head_dim,
+                          alpha=wl.alpha)
+        for form, g in gpu.items():
+            es = _rel(g["sigma"][l], ref["sigma"][0]).max()
+            ec = float(_rel(g["scale"][l], ref["scale"][0]))
+            cos = np.abs(np.sum(g["v"][l].astype(np.float64) * ref["v"][0], axis=-1)).min()
+            assert es <= RTOL and ec <= RTOL, (form, l, es, ec)
+            np.testing.assert_array_equal(g["iters"][l], ref["iters"][0])
+            assert cos >= 1 - 1e-3, (form, l, cos)
+            w = worst[form]
+            w[0], w[1], w[2] = max(w[0], es), max(w[1], ec), min(w[2], cos)
+        for (ls, h) in sample:   # the explicit route on the seeded sample of this layer
+            if ls != l:
+                continue
+            WQ, WK = head_slices(wq_l, wk_l, h, wl.n_kv, wl.head_dim)
+            sig_e, _, _, it_e = dense_power_iteration(interaction_matrix(WQ, WK), v0c[l, h], wl.n_iter)
+            assert it_e == wl.n_iter
+            for form, g in gpu.items():
+                e = float(_rel(g["sigma"][l, h], sig_e))
+                assert e <= RTOL, (form, l, h, e)
+                e_worst = max(e_worst, e)
+    print(f"{key}: all {wl.n_heads} heads and {wl.n_layers} scales, "
+          + ", ".join(f"{f}: sigma {w[0]:.2e} scale {w[1]:.2e} min|cos v| {w[2]:.6f}" for f, w in worst.items())
+          + f"; explicit-M sample of {len(sample)} heads: {e_worst:.2e}")
     del gq, gk
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("form", FORMS)
+def test_small_configs_against_the_explicit_route(form):
+    """Every head of the tiny check (sweep chain only: d_h = 8) and of the
+    GPT-2-small shape against the explicit route: M formed in float64, dense
+    power iteration (the oracle's textbook cross-check), u and v by cosine,
+    and the per-layer scale from the largest explicit sigma."""
+    from oracle.explicit import dense_power_iteration, interaction_matrix
+    for key in ("tiny", "gpt2-small"):
+        wl = WORKLOADS[key]
+        if form == "gram" and wl.head_dim < 16:
+            continue
+        wq, wk, v0, gq, gk = _cpu_case(wl)
+        gpu = run_gpu(wl, gq, gk, v0, wl.n_iter, want_u=True, flags=FORMS[form])
+        wq_n, wk_n = _np(wq), _np(wk)
+        worst = 0.0
+        for l in range(wl.n_layers):
+            sig_l = []
+            for h in range(wl.n_q):
+                WQ, WK = head_slices(wq_n[l], wk_n[l], h, wl.n_kv, wl.head_dim)
+                sig, u, v, it = dense_power_iteration(interaction_matrix(WQ, WK), v0[l, h].double().numpy(), wl.n_iter)
+                e = float(_rel(gpu["sigma"][l, h], sig))
+                assert e <= RTOL and gpu["iters"][l, h] == it, (key, l, h, e)
+                assert abs(gpu["v"][l, h] @ v) >= 1 - 1e-3 and abs(gpu["u"][l, h] @ u) >= 1 - 1e-3
+                worst = max(worst, e)
+                sig_l.append(sig)
+            assert _rel(gpu["scale"][l], layer_scale(max(sig_l), wl.alpha, wl.d_model, wl.head_dim)) <= RTOL
+        print(f"{key} ({form}): every head against the explicit route, max rel err {worst:.2e}")
 
 
 def _check_tolerance_stop(res_gpu_iters, res_gpu_sigma, WQ, WK, v_start, tol, cap, eps=0.1):

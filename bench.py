@@ -28,9 +28,24 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E, vendor figure
+# what `dtype` ("f32") summarises: the arithmetic of each form's kernels
+ARITHMETIC = {
+    "chain": "W_Q sweep: fp32 FMA on the weights (bf16 widened exactly); W_K sweep of grouped bf16 heads (3..8 query "
+             "heads per key head, d_h 64/128): bf16 matrix-core products of K with each fp32 vector split into hi and "
+             "lo bf16 halves (about 16 significant bits), fp32 accumulation; other W_K sweeps fp32 FMA; norms, "
+             "normalisation and the scale fp32",
+    "gram": "Gram matrices: bf16 (fp32: fp32) matrix-core products, fp32 accumulation; d_h-space iteration, norms "
+            "and the scale fp32; final sweeps as in the chain",
+    "layer": "fp32 FMA on the weights (bf16 widened exactly), fp32 norms and scale",
+}
 METRIC = "heads·iters/sec (all layers) and achieved HBM GB/s vs MI355X peak"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "q_sweep_traffic.json")
 KERNEL_DIR = os.path.join(ROOT, "paper_2602_18851_amd", "csrc")
+
+
+def log(msg: str) -> None:
+    """Progress of the run on stderr (the JSON line alone goes to stdout)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def parse():
@@ -59,6 +74,10 @@ def parse():
                    help="copy: one plain device copy of --copy-bytes, the reference for HBM byte counters; "
                         "perstep: only the per-step recompute scenario (its JSON line), in the --form chosen")
     p.add_argument("--copy-bytes", type=int, default=4 << 30)
+    p.add_argument("--flush", action="store_true",
+                   help="chain/gram forms: before every timed call write a 1 GiB scratch buffer (evicts L2 and the "
+                        "256 MB Infinity Cache), each call timed alone by HIP events")
+    p.add_argument("--calib-steps", type=int, default=20, help="fp8 form: auto-alpha burn-in steps")
     return p.parse_args()
 
 
@@ -126,6 +145,20 @@ def measured_traffic(kernel: str = ""):
     return (t.get(kernel) or {}).get("bytes_per_launch") if kernel else t.get("bytes_per_launch")
 
 
+def host_info() -> dict:
+    """The host the CPU baseline ran on: logical CPUs and the CPU model."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"os_cpu_count": os.cpu_count(), "cpu_model": model}
+
+
 def cpu_baseline(wl, budget_s: float, n_iter: int):
     """The float64 oracle (per head, the paper's step order) on host cores,
     over as many heads of the workload as fit in the time budget."""
@@ -154,6 +187,8 @@ def cpu_baseline(wl, budget_s: float, n_iter: int):
         "kind": "oracle",
         "sample": f"{heads} head estimates cycling over the {wl.n_q} query heads of layer 0, {n_iter} iterations "
                   f"each, float64 numpy (implicit 4-GEMV chain per head), {dt:.1f} s",
+        "cores_note": "cores = BLAS threads the oracle ran with",
+        **host_info(),
     }
 
 
@@ -202,7 +237,8 @@ def cpu_baseline_layer(wl, budget_s: float, n_iter: int):
     dt = time.perf_counter() - t0
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {"value": runs * n_iter / dt, "unit": "layers·iters/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{runs} runs of the layer-0 estimator, {n_iter} iterations each, float64 numpy, {dt:.1f} s"}
+            "sample": f"{runs} runs of the layer-0 estimator, {n_iter} iterations each, float64 numpy, {dt:.1f} s",
+            **host_info()}
 
 
 def cpu_baseline_fp8(wl, budget_s: float, seq: int):
@@ -226,7 +262,7 @@ def cpu_baseline_fp8(wl, budget_s: float, seq: int):
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {"value": heads * seq * seq / dt, "unit": "scaled logits/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{heads} heads of layer 0 ({seq} tokens: projections, logits, E4M3 codes, counts), "
-                      f"float64 numpy, {dt:.1f} s"}
+                      f"float64 numpy, {dt:.1f} s", **host_info()}
 
 
 def context_lines(args, flags: int) -> dict:
@@ -383,6 +419,7 @@ def bench_fp8(args):
         spectral_logits_fp8(est.ctx, xs, wl.d_model, seq, wqs, wks, scale.data_ptr(), ws.data_ptr(), ws.numel(),
                             codes.data_ptr(), max_abs.data_ptr(), n_over.data_ptr())
 
+    log(f"{wl.key} fp8 consumer: warm-up {args.warmup}, then {args.steps} timed calls")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -426,11 +463,104 @@ def bench_fp8(args):
             "logits_kernel_TFLOPs": logit_flops / (l_ms / max(l_n - 1, 1) * 1e-3) / 1e12,
         },
     }
+    from paper_2602_18851_amd import fp8_report
+    out["report"] = dict(fp8_report(max_abs, n_over), scale=f"Eq. scale, alpha {wl.alpha}, {wl.n_iter} cold "
+                                                             f"iterations (Gram form)")
     if not args.no_extras:
         out["context"] = {"library_gemm": library_projection(x, wq, wk, proj_flops)}
+        del wq, wk, x, codes, ws
+        est.close()
+        torch.cuda.empty_cache()
+        out["context"]["auto_alpha"] = auto_alpha_burnin(wl, seq, args.calib_steps)
+        out["context"]["pretrained_analogue"] = pretrained_analogue(seq)
     if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
         out["cpu_baseline"] = cpu_baseline_fp8(wl, args.cpu_seconds, seq)
     print(json.dumps(out), flush=True)
+
+
+def auto_alpha_burnin(wl, seq: int, steps: int, quantile: float = 0.9999, kappa: float = 1.0) -> dict:
+    """Auto-alpha (Sec. 3.5; App. M, Algorithm "Auto-alpha Calibration") on
+    the workload: cold start (five iterations, the paper's count), then
+    `steps` burn-in steps, each a seeded perturbation of the weights, one warm
+    estimator iteration (the paper's steady state) at the conservative
+    alpha_0 = the workload's alpha, and the E4M3 consumer on fresh seeded
+    tokens; the slack ratios (one per layer and step) give alpha_final, and
+    one more step at alpha_final shows the utilisation it buys."""
+    import numpy as np
+    import torch
+
+    from paper_2602_18851_amd import AutoAlpha, Spectral, fp8_report
+    from paper_2602_18851_amd.spectral import spectral_logits_workspace_bytes
+    from workloads import all_weights, device_tokens, start_vectors
+
+    dev = torch.device("cuda", 0)
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha)
+    ws = torch.empty(spectral_logits_workspace_bytes(est.shape, seq), dtype=torch.uint8, device=dev)
+    wq, wk = all_weights(wl, dev)
+    v = start_vectors(wl, dev)
+    est.step(wq, wk, v, 5)
+    auto = AutoAlpha(wl.d_model, wl.head_dim, quantile, kappa)
+    util0 = []
+    t0 = time.perf_counter()
+    for t in range(steps):
+        log(f"auto-alpha burn-in step {t + 1}/{steps}")
+        del wq, wk
+        wq, wk = all_weights(wl, dev, perturbed=True, step=t)
+        x = device_tokens(wl, seq, dev, step=t)
+        sigma, scale, _ = est.step(wq, wk, v, 1)
+        max_abs, n_over, _ = est.logits_fp8(x, wq, wk, scale, workspace=ws)
+        auto.observe(sigma, scale, max_abs)
+        util0.append(fp8_report(max_abs, n_over)["utilization_pct_layers"]["median"])
+    alpha = auto.alpha()
+    est.close()
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, alpha)
+    del wq, wk
+    wq, wk = all_weights(wl, dev, perturbed=True, step=steps)
+    x = device_tokens(wl, seq, dev, step=steps)
+    _, scale, _ = est.step(wq, wk, v, 1)
+    max_abs, n_over, _ = est.logits_fp8(x, wq, wk, scale, workspace=ws)
+    after = fp8_report(max_abs, n_over)
+    est.close()
+    r = np.asarray(auto.ratios)
+    return {"alpha_0": wl.alpha, "burn_in_steps": steps, "quantile": quantile, "kappa": kappa,
+            "slack_ratios": {"n": int(r.size), "min": float(r.min()), "max": float(r.max()), "mean": float(r.mean())},
+            "alpha_final": alpha, "tightening": wl.alpha / alpha,
+            "utilization_pct_median_at_alpha_0": float(np.median(util0)),
+            "next_step_at_alpha_final": after, "wall_s": time.perf_counter() - t0,
+            "note": "one slack ratio per layer and step: max|S| of the layer's heads over B_max = sigma_l d / sqrt(d_h)"}
+
+
+def pretrained_analogue(seq: int) -> dict:
+    """Table "pretrained" and App. J analogues on the synthetic GPT-2-XL,
+    Llama-2-7B and 70B shapes: the estimator's own scale (the workload's
+    alpha, its cold iteration count) on the first call, then the E4M3
+    consumer on `seq` post-normalisation tokens per layer: layers with an
+    overflow, the largest scaled logit, and the utilisation."""
+    import torch
+
+    from paper_2602_18851_amd import Spectral, fp8_report
+    from paper_2602_18851_amd.spectral import SN_FLAG_GRAM
+    from workloads import WORKLOADS, all_weights, device_tokens, start_vectors
+
+    dev = torch.device("cuda", 0)
+    out = {}
+    for key in ("gpt2-xl", "llama2-7b-spiked", "llama2-70b-gqa"):
+        log(f"pretrained analogue: {key}")
+        wl = WORKLOADS[key]
+        wq, wk = all_weights(wl, dev)
+        x = device_tokens(wl, seq, dev)
+        est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha,
+                       flags=SN_FLAG_GRAM)
+        _, scale, _ = est.step(wq, wk, start_vectors(wl, dev), wl.n_iter)
+        max_abs, n_over, _ = est.logits_fp8(x, wq, wk, scale)
+        rep = fp8_report(max_abs, n_over)
+        out[key] = {"overflow": f"{rep['overflow_layers']}/{rep['layers']}", "max_scaled": rep["max_scaled"],
+                    "alpha": wl.alpha, "n_iter": wl.n_iter, **rep}
+        est.close()
+        del wq, wk, x
+        torch.cuda.empty_cache()
+    return out
 
 
 def library_projection(x, wq, wk, flops: float) -> dict:
@@ -505,6 +635,7 @@ def main():
         else:
             est.step(wq, wk, v, n_iter, sigma=sigma, scale=scale, iters=iters)
 
+    log(f"{wl.key} ({args.form}): warm-up {args.warmup}, then {args.steps} timed calls")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -520,14 +651,30 @@ def main():
             timed_step()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    t_wall = time.perf_counter()
-    e0.record()
-    for _ in range(args.steps):
-        timed_step()
-    e1.record()
-    torch.cuda.synchronize()
-    wall_s = time.perf_counter() - t_wall
-    ms = e0.elapsed_time(e1) / args.steps
+    if args.flush:
+        # every call starts from cold caches: 1 GiB written first (4x the
+        # Infinity Cache), each call timed alone between its own events
+        scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        t_wall = time.perf_counter()
+        for k, (a_, b_) in enumerate(evs):
+            scratch.fill_(k & 0xFF)
+            a_.record()
+            timed_step()
+            b_.record()
+        torch.cuda.synchronize()
+        wall_s = time.perf_counter() - t_wall
+        ms = sum(a_.elapsed_time(b_) for a_, b_ in evs) / args.steps
+        del scratch
+    else:
+        t_wall = time.perf_counter()
+        e0.record()
+        for _ in range(args.steps):
+            timed_step()
+        e1.record()
+        torch.cuda.synchronize()
+        wall_s = time.perf_counter() - t_wall
+        ms = e0.elapsed_time(e1) / args.steps
     assert bool(torch.isfinite(sigma).all()) and (layer or bool((iters == n_iter).all()))
 
     # per-kernel durations, HIP events on the launch stream (separate pass)
@@ -596,7 +743,10 @@ def main():
             "start": "cold (seeded unit vectors), state carried across steps",
             "form": args.form,
             "launch": "HIP graph replay" if args.graph and not layer else "eager",
+            "cache": "1 GiB written before every timed call, calls timed one by one" if args.flush
+                     else "calls back to back, no flush",
         },
+        "arithmetic": ARITHMETIC["gram" if gram else "layer" if layer else "chain"],
         "effective_GBps": call_bytes / (ms * 1e-3) / 1e9,
         "effective_frac_of_peak": call_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "call_bytes": call_bytes,
@@ -620,11 +770,13 @@ def main():
         out["roofline"]["mfma_frac_of_dense_peak"] = out["roofline"]["mfma_TFLOPs"] / (2500.0 if wl.dtype == "bf16"
                                                                                         else 157.3)
     if not layer and not args.no_extras:
+        log("context lines")
         del wq, wk
         est.close()
         torch.cuda.empty_cache()
         out["context"] = context_lines(args, flags)
     if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
         out["cpu_baseline"] = (cpu_baseline_layer if layer else cpu_baseline)(wl, args.cpu_seconds, n_iter)
         if not layer and not gram and not args.no_extras:
             out.setdefault("context", {})["oracle_explicit_M"] = cpu_explicit_m(wl, args.cpu_seconds / 3, n_iter)

@@ -251,6 +251,68 @@ def spectral_logits_fp8(ctx: int, x_ptrs: Sequence[int], ld_x: int, seq_len: int
                                               ctypes.c_void_p(max_abs), ctypes.c_void_p(n_over)))
 
 
+# ------------------------------------------- consumer-side calibration
+
+
+class AutoAlpha:
+    """Auto-alpha calibration (Sec. 3.5; App. M, Algorithm "Auto-alpha
+    Calibration") driven by the FP8 consumer.  Each burn-in step observes,
+    per layer l, the largest logit M = max_h max|S~_h| * scale_l (the
+    consumer's max_abs times the scale it divided by) and the bound
+    B_max = sigma^(l) d / sqrt(d_h), sigma^(l) = max_h sigma_h of the step's
+    estimate, and records r = M / B_max (spectral_slack_ratio).  alpha()
+    returns Quantile_q(R) * kappa (spectral_auto_alpha).  Layers whose sigma
+    or scale is not finite and positive (degenerate heads) are skipped."""
+
+    def __init__(self, d_model: int, head_dim: int, quantile: float = 0.9999, kappa: float = 1.0):
+        self.d_model, self.head_dim = int(d_model), int(head_dim)
+        self.quantile, self.kappa = float(quantile), float(kappa)
+        self.ratios: list[float] = []
+
+    def observe(self, sigma, scale, max_abs) -> list[float]:
+        """sigma [L, n_q], scale [L], max_abs [L, n_q] (tensors or arrays) of
+        one step; returns the step's ratios, one per layer."""
+        import numpy as np
+
+        def host(t):
+            return np.asarray(t.detach().double().cpu().numpy() if hasattr(t, "detach") else t, dtype=np.float64)
+
+        sig, sc, mx = host(sigma), host(scale), host(max_abs)
+        out = []
+        for l in range(sc.shape[0]):
+            s_l, m_l = float(sig[l].max()), float(mx[l].max())
+            if not (np.isfinite(s_l) and s_l > 0 and np.isfinite(sc[l]) and sc[l] > 0 and np.isfinite(m_l)):
+                continue
+            out.append(spectral_slack_ratio(m_l * float(sc[l]), s_l, self.d_model, self.head_dim))
+        self.ratios.extend(out)
+        return out
+
+    def alpha(self) -> float:
+        return spectral_auto_alpha(self.ratios, self.quantile, self.kappa)
+
+
+def fp8_report(max_abs, n_over, r_max: float = 448.0) -> dict:
+    """Statistics of one consumer call in the form of the paper's tables:
+    layers with any logit past R_max (Table "pretrained", "Overflow") and the
+    largest scaled logit ("Max Scaled"); FP8 range utilisation max|S~| / R_max
+    (Sec. 1), per layer (its largest head) and per head, as median, P10 and
+    P90 in percent (App. J, Table "utilization_app")."""
+    import numpy as np
+
+    mx = np.asarray(max_abs.detach().double().cpu().numpy() if hasattr(max_abs, "detach") else max_abs,
+                    dtype=np.float64)
+    ov = np.asarray(n_over.detach().cpu().numpy() if hasattr(n_over, "detach") else n_over)
+    per_layer = 100.0 * mx.max(axis=1) / r_max
+    per_head = 100.0 * mx.reshape(-1) / r_max
+
+    def q(a):
+        return {"median": float(np.median(a)), "p10": float(np.percentile(a, 10)), "p90": float(np.percentile(a, 90))}
+
+    return {"overflow_layers": int((ov.reshape(ov.shape[0], -1) > 0).any(axis=1).sum()), "layers": int(mx.shape[0]),
+            "overflow_logits": int(ov.sum()), "max_scaled": float(mx.max()),
+            "utilization_pct_layers": q(per_layer), "utilization_pct_heads": q(per_head)}
+
+
 # ----------------------------------------------------------- torch wrapper
 
 

@@ -27,7 +27,7 @@ pytestmark = pytest.mark.gpu
 if not torch.cuda.is_available():  # pragma: no cover - collected on CPU machines, skipped there
     pytest.skip("needs a GPU", allow_module_level=True)
 
-from paper_2602_18851_amd import Spectral  # noqa: E402
+from paper_2602_18851_amd import Spectral, fp8_report  # noqa: E402
 
 TAU = 2.0 ** -14
 
@@ -234,4 +234,45 @@ def test_separate_layer_buffers_and_several_row_tiles():
             check_head(codes[l, h], max_abs[l, h], n_over[l, h], xs[l], wq[l], wk[l], s32[l], h, wl.n_kv,
                        wl.head_dim)
     assert n_over.sum() > 0
+    est.close()
+
+
+def test_report_lines_on_the_gpt2_xl_shape_against_the_oracle():
+    """Table "pretrained" and App. J analogues on the GPT-2-XL shape: the
+    estimator's own scale (alpha 0.08, 30 cold iterations), 1024
+    post-normalisation tokens per layer, every layer on the GPU; the per-layer
+    utilisation max|S~| / 448 and overflow flag of two seeded layers (all
+    heads) against the oracle's logits at the oracle's own scale, and the
+    report's fields against the per-layer values they summarise."""
+    from oracle.power_iteration import spectral_step as oracle_step
+    from workloads import start_vectors
+    wl = WORKLOADS["gpt2-xl"]
+    seq = 1024
+    gq, gk = all_weights(wl, "cuda")
+    x = torch.stack([layer_tokens(wl, seq, l) for l in range(wl.n_layers)]).cuda()
+    v0 = start_vectors(wl, "cuda")
+    est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha)
+    _, scale, _ = est.step(gq, gk, v0.clone(), wl.n_iter)
+    max_abs, n_over, _ = est.logits_fp8(x, gq, gk, scale)
+    rep = fp8_report(max_abs, n_over)
+    mx, ov = max_abs.double().cpu().numpy(), n_over.cpu().numpy()
+    util = 100.0 * mx.max(axis=1) / 448.0
+    assert rep["layers"] == wl.n_layers and rep["overflow_layers"] == int((ov > 0).any(axis=1).sum())
+    assert rep["max_scaled"] == pytest.approx(mx.max())
+    assert rep["utilization_pct_layers"]["median"] == pytest.approx(np.median(util))
+    assert rep["utilization_pct_layers"]["p10"] <= rep["utilization_pct_layers"]["median"] <= \
+        rep["utilization_pct_layers"]["p90"]
+    rng = np.random.default_rng(wl.cfg_id)
+    v0c = v0.double().cpu().numpy()
+    for l in sorted(rng.choice(wl.n_layers, 2, replace=False)):
+        wq_l, wk_l, x_l = gq[l].double().cpu().numpy(), gk[l].double().cpu().numpy(), x[l].double().cpu().numpy()
+        ref = oracle_step([wq_l], [wk_l], v0c[l:l + 1], wl.n_iter, n_kv=wl.n_kv, head_dim=wl.head_dim,
+                          alpha=wl.alpha)
+        res = fp8_consumer.consume_layer(x_l, wq_l, wk_l, ref["scale"][0], wl.n_kv, wl.head_dim, want_codes=False)
+        u_ref = 100.0 * max(res["max_abs"].values()) / 448.0
+        assert abs(util[l] - u_ref) <= 1e-3 * u_ref, (l, util[l], u_ref)
+        assert (ov[l] > 0).any() == (max(res["n_over"].values()) > 0)
+    print(f"gpt2-xl: overflow layers {rep['overflow_layers']}/{rep['layers']}, max scaled {rep['max_scaled']:.1f}, "
+          f"utilisation per layer median {rep['utilization_pct_layers']['median']:.2f} % "
+          f"(P10 {rep['utilization_pct_layers']['p10']:.2f}, P90 {rep['utilization_pct_layers']['p90']:.2f})")
     est.close()

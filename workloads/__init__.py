@@ -14,6 +14,7 @@ from .synth import (  # noqa: F401
     layer_start_vectors,
     perturb_master,
     tokens,
+    device_tokens,
     planted_singular_values,
     seed_of,
 )

@@ -108,8 +108,11 @@ WORKLOADS: dict[str, Workload] = {
 }
 
 
-def seed_of(cfg_id: int, layer: int, stream: str) -> int:
-    ss = np.random.SeedSequence([SEED_ROOT, int(cfg_id), int(layer), STREAMS[stream]])
+def seed_of(cfg_id: int, layer: int, stream: str, step: int | None = None) -> int:
+    """Seed of one (config, layer, stream); ``step`` (a burn-in step) extends
+    the sequence so that every step draws afresh."""
+    key = [SEED_ROOT, int(cfg_id), int(layer), STREAMS[stream]] + ([] if step is None else [int(step)])
+    ss = np.random.SeedSequence(key)
     return int(ss.generate_state(1, dtype=np.uint64)[0] & np.uint64((1 << 62) - 1))
 
 
@@ -119,8 +122,9 @@ def _gen(device, seed: int) -> torch.Generator:
     return g
 
 
-def _np_rng(cfg_id: int, layer: int, stream: str) -> np.random.Generator:
-    return np.random.default_rng(np.random.SeedSequence([SEED_ROOT, int(cfg_id), int(layer), STREAMS[stream]]))
+def _np_rng(cfg_id: int, layer: int, stream: str, step: int | None = None) -> np.random.Generator:
+    key = [SEED_ROOT, int(cfg_id), int(layer), STREAMS[stream]] + ([] if step is None else [int(step)])
+    return np.random.default_rng(np.random.SeedSequence(key))
 
 
 def bf16_round(t: torch.Tensor) -> torch.Tensor:
@@ -214,30 +218,33 @@ def _store(t32: torch.Tensor, wl: Workload) -> torch.Tensor:
     return t32.to(wl.torch_dtype)
 
 
-def perturb_master(wl: Workload, layer: int, wq: torch.Tensor, wk: torch.Tensor):
-    """W <- W + 1e-3 * N(0,1) * ||W||_F / sqrt(numel), per layer tensor (float32 masters)."""
+def perturb_master(wl: Workload, layer: int, wq: torch.Tensor, wk: torch.Tensor, step: int | None = None):
+    """W <- W + 1e-3 * N(0,1) * ||W||_F / sqrt(numel), per layer tensor (float32 masters);
+    ``step`` draws the perturbation of one burn-in step."""
     out = []
     for which, w in (("q", wq), ("k", wk)):
-        g = _gen(w.device, seed_of(wl.cfg_id, layer, "perturb") + (0 if which == "q" else 1))
+        g = _gen(w.device, seed_of(wl.cfg_id, layer, "perturb", step) + (0 if which == "q" else 1))
         rms = torch.sqrt(torch.mean(w.double() ** 2)).item()
         out.append(w + torch.randn(w.shape, generator=g, device=w.device, dtype=torch.float32) * (1e-3 * rms))
     return out[0], out[1]
 
 
-def layer_weights(wl: Workload, layer: int, device="cpu", perturbed: bool = False):
+def layer_weights(wl: Workload, layer: int, device="cpu", perturbed: bool = False, step: int | None = None):
+    """Storage-dtype weights of one layer; ``perturbed`` adds the seeded
+    perturbation (of burn-in step ``step`` if given) to the float32 master."""
     wq, wk = layer_master(wl, layer, device)
     if perturbed:
-        wq, wk = perturb_master(wl, layer, wq, wk)
+        wq, wk = perturb_master(wl, layer, wq, wk, step)
     return _store(wq, wl), _store(wk, wl)
 
 
-def all_weights(wl: Workload, device="cpu", perturbed: bool = False):
+def all_weights(wl: Workload, device="cpu", perturbed: bool = False, step: int | None = None):
     """Stacked storage-dtype weights: wq [L, n_q*d_h, d], wk [L, n_kv*d_h, d]."""
     L, d, dh = wl.n_layers, wl.d_model, wl.head_dim
     wq = torch.empty(L, wl.n_q * dh, d, dtype=wl.torch_dtype, device=device)
     wk = torch.empty(L, wl.n_kv * dh, d, dtype=wl.torch_dtype, device=device)
     for layer in range(L):
-        q, k = layer_weights(wl, layer, device, perturbed)
+        q, k = layer_weights(wl, layer, device, perturbed, step)
         wq[layer].copy_(q)
         wk[layer].copy_(k)
         del q, k
@@ -262,10 +269,24 @@ def layer_start_vectors(wl: Workload, device="cpu") -> torch.Tensor:
     return v.to(torch.float32)
 
 
-def tokens(wl: Workload, n: int, spherical: bool = False, layer: int = 0) -> np.ndarray:
+def tokens(wl: Workload, n: int, spherical: bool = False, layer: int = 0, step: int | None = None) -> np.ndarray:
     """Token embeddings x_i ~ N(0, I_d) (float64, CPU); ``spherical`` rescales
-    every row to norm sqrt(d), the post-normalisation model of Sec. 3.2."""
-    x = _np_rng(wl.cfg_id, layer, "x").standard_normal((n, wl.d_model))
+    every row to norm sqrt(d), the post-normalisation model of Sec. 3.2;
+    ``step`` draws the tokens of one burn-in step."""
+    x = _np_rng(wl.cfg_id, layer, "x", step).standard_normal((n, wl.d_model))
     if spherical:
         x *= math.sqrt(wl.d_model) / np.linalg.norm(x, axis=1, keepdims=True)
     return x
+
+
+def device_tokens(wl: Workload, n: int, device, step: int | None = None) -> torch.Tensor:
+    """Post-normalisation tokens of every layer drawn on ``device`` (a torch
+    generator, so not the draws of ``tokens``): x = sqrt(d) u, u uniform on the
+    sphere, bf16 [L, n, d]."""
+    out = torch.empty(wl.n_layers, n, wl.d_model, dtype=torch.bfloat16, device=device)
+    for layer in range(wl.n_layers):
+        x = torch.randn(n, wl.d_model, generator=_gen(device, seed_of(wl.cfg_id, layer, "x", step)), device=device,
+                        dtype=torch.float32)
+        x *= math.sqrt(wl.d_model) / torch.linalg.vector_norm(x, dim=1, keepdim=True)
+        out[layer].copy_(x)
+    return out

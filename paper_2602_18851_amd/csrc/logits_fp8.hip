@@ -21,6 +21,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <type_traits>
 
 #include "device_util.h"
 #include "logits_fp8.h"
@@ -29,8 +30,6 @@ namespace {
 
 using namespace sn_dev;
 
-constexpr int kWaves = 4;      // logit kernel: 2 x 2 waves of 64 x 64 per 128 x 128 tile
-constexpr int kTile = 128;
 
 __device__ __forceinline__ f32x4 mfma(const u32x4& a, const u32x4& b, const f32x4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
@@ -145,135 +144,259 @@ __global__ void __launch_bounds__(64 * kPWaves) __attribute__((amdgpu_waves_per_
       }
 }
 
-// Logits of all layers in one launch: one 128 x 128 tile of S of one query
-// head of one layer per workgroup, 64 x 64 per wave.  The workgroup stages the hi and lo planes of
-// its 128 query rows and 128 key rows through LDS, 64 columns of d_h at a
-// time (coalesced loads; see stage_issue), and every wave reads its operands
-// back in the MFMA layout.  The products are formed transposed (A = key
-// rows, B = query rows), so a lane holds 4 consecutive columns of one row of
-// S: one 32-bit word of E4M3 codes.  v_cvt_pk_fp8_f32 (no clamp) rounds to
+// Logits of all layers in one launch.  A workgroup owns 128 queries of one
+// query head of one layer and walks every key tile of its key head: 4 waves,
+// wave w computing queries 32 w .. 32 w + 31 against the 64 keys of a tile
+// as two 32 x 32 blocks of v_mfma_f32_32x32x16_bf16.  With 64 KB of LDS per
+// workgroup, two run on each CU (two waves per SIMD), so one's set-up and
+// epilogue overlap the other's products.  The products are
+// formed transposed (A = key rows, B = query rows): a lane then holds 4
+// consecutive keys of one query row of S, one 32-bit word of E4M3 codes.
+//   - The wave's B operands (its 32 query rows, hi and lo planes, all of d_h)
+//     are loaded once, through LDS, and stay in registers.
+//   - Key tiles (64 rows x d_h, hi and lo) stream through two LDS stages:
+//     the loads of tile t + 1 are issued before tile t is multiplied.
+//   - The codes of tile t are stored while tile t + 1 is multiplied, so the
+//     wait for a stage never covers fresh stores.
+// LDS rows hold their 16-byte chunks swizzled, chunk c of row r at slot
+// c ^ f(r), f(r) = (r / (16 / CH)) mod CH for CH chunks per row: the 16
+// lanes of a 16-byte operand read (16 consecutive rows, one chunk) then hit
+// 16 distinct groups of 4 banks.  v_cvt_pk_fp8_f32 (no clamp) rounds to
 // nearest even and gives the NaN code past 464, the OCP E4M3FN conversion the
 // oracle defines; a bit-by-bit comparison with an integer encoder over every
 // rounding point and 400k random values in [-600, 600] found no difference
 // for non-NaN inputs.
-constexpr int kPlaneBytes = kTile * 128;  // 128 rows x 64 columns of one bf16 plane
+constexpr int kLQ = 128;     // queries per workgroup
+constexpr int kLWaves = 4;   // 32 queries each
+constexpr int kLK = 64;      // keys per tile
+constexpr int kLMB = kLK / 32;  // 32-key blocks per tile
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 template <int DH>
-__global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
-  constexpr int NSTEP = (DH + 63) / 64;  // 64-column steps over d_h
-  __shared__ __attribute__((aligned(16))) uint8_t stage[4 * kPlaneBytes];  // Q hi, Q lo, K hi, K lo
+struct LogitShape {
+  static constexpr int RB = 2 * DH;           // bytes of one row of one plane
+  static constexpr int CH = RB / 16;          // 16-byte chunks per row
+  static constexpr int RPI = 1024 / RB;       // rows per 64-lane staging instruction
+  static constexpr int PLANE_K = kLK * RB;    // one plane of a key tile
+  static constexpr int TILE = 2 * PLANE_K;    // hi and lo planes
+  static constexpr int KB = DH / 16;          // k blocks of 16
+};
+
+template <int DH>
+__device__ __forceinline__ int lswz(int r) {
+  constexpr int CH = LogitShape<DH>::CH;
+  return (r / (16 / CH)) & (CH - 1);
+}
+
+// Issues this wave's share of the loads of R rows (rows row0 .. row0 + R - 1
+// of the resource, row r at byte r * stride) of the hi and lo planes into LDS
+// (plane p at lds + p * R * RB), swizzled; 64-lane instructions J = wave,
+// wave + kLWaves, ... over the 2 * R * RB / 1024 of them.
+template <int DH, int R>
+__device__ __forceinline__ void lstage(__amdgpu_buffer_rsrc_t hi, __amdgpu_buffer_rsrc_t lo, uint8_t* lds, int row0,
+                                       uint32_t stride, int wave, int lane) {
+  using S = LogitShape<DH>;
+  constexpr int N_INS = R * S::RB / 1024;  // per plane
+  static_assert((2 * N_INS) % kLWaves == 0, "staging instructions split evenly over the waves");
+#pragma unroll
+  for (int jj = 0; jj < 2 * N_INS / kLWaves; ++jj) {
+    const int J = wave + kLWaves * jj;
+    const int plane = J / N_INS, jp = J % N_INS;
+    const int row = jp * S::RPI + lane / S::CH;
+    const int c = (lane % S::CH) ^ lswz<DH>(row);
+    const uint32_t voff = (uint32_t)(row0 + row) * stride + 16u * (uint32_t)c;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(plane ? lo : hi, (lds_void*)(lds + plane * R * S::RB + 1024 * jp), 16,
+                                             voff, 0, 0, 0);
+  }
+}
+
+// 16-byte chunk c of row r of a staged plane.
+template <int DH>
+__device__ __forceinline__ u32x4 lchunk(const uint8_t* plane, int r, int c) {
+  return *reinterpret_cast<const u32x4*>(plane + r * LogitShape<DH>::RB + 16 * (c ^ lswz<DH>(r)));
+}
+
+__device__ __forceinline__ f32x16 mfma32(const u32x4& a, const u32x4& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                 0, 0);
+}
+
+template <int DH>
+__global__ void __launch_bounds__(64 * kLWaves) __attribute__((amdgpu_waves_per_eu(2, 2))) logits_kernel(LogitArgs a) {
+  using S = LogitShape<DH>;
+  constexpr int KB = S::KB;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * S::TILE];  // two key stages; first the query tile
+  static_assert(2 * kLQ * S::RB == 2 * S::TILE, "the query tile fills both key stages");
   const int lane = threadIdx.x & 63;
   const int wv = uni((int)(threadIdx.x >> 6));
-  const int q = lane >> 4, s = lane & 15;
-  // consecutive tiles (one head after another, the heads of a key group in
-  // turn) run on one XCD and share its L2
-  const int per_head = a.tiles * a.tiles;
+  const int hl = lane >> 5, n = lane & 31;
+  // consecutive workgroups (the heads of one key group, then their query
+  // tiles) run on one XCD and share its L2
+  const int n_qt = (a.seq + kLQ - 1) / kLQ;
   const int per_xcd = gridDim.x / 8;
   const int bl = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (bl >= a.layers * a.n_heads * per_head) return;  // whole workgroup
-  const int layer = bl / (a.n_heads * per_head), b = bl % (a.n_heads * per_head);
-  const int h = b / per_head;
-  const int ti = (b % per_head) / a.tiles, tj = b % a.tiles;
-  const int kvh = h / a.g;
-  const int wm = wv >> 1, wn = wv & 1;
-  const int i0 = ti * kTile + 64 * wm, j0 = tj * kTile + 64 * wn;  // this wave's rows of S
+  if (bl >= a.layers * a.n_heads * n_qt) return;  // whole workgroup
+  const int qt = bl % n_qt, lh = bl / n_qt;       // lh = layer * n_heads + h
+  const int layer = lh / a.n_heads, h = lh % a.n_heads, kvh = h / a.g;
+  const int q0 = qt * kLQ;
 
-  // this wave stages rows 32 wv .. 32 wv + 31 of the four planes
-  const int qr = ti * kTile + 32 * wv, kr = tj * kTile + 32 * wv;
-  const int64_t q_len = qr < a.seq ? (((int64_t)(a.seq - 1 - qr) * a.nq_cols + DH) * 2 + 15) & ~int64_t(15) : 0;
-  const int64_t k_len = kr < a.seq ? (((int64_t)(a.seq - 1 - kr) * a.nk_cols + DH) * 2 + 15) & ~int64_t(15) : 0;
-  const size_t qo = ((size_t)layer * a.seq + qr) * a.nq_cols + (size_t)h * DH;
-  const size_t ko = ((size_t)layer * a.seq + kr) * a.nk_cols + (size_t)kvh * DH;
-  const __amdgpu_buffer_rsrc_t rqh = make_rsrc(a.qh + qo, (uint32_t)q_len), rql = make_rsrc(a.ql + qo, (uint32_t)q_len);
-  const __amdgpu_buffer_rsrc_t rkh = make_rsrc(a.kh + ko, (uint32_t)k_len), rkl = make_rsrc(a.kl + ko, (uint32_t)k_len);
-  const uint32_t q_rb = (uint32_t)(a.nq_cols * 2), k_rb = (uint32_t)(a.nk_cols * 2);
-  auto issue = [&](int st) {
-    const uint32_t col = (uint32_t)(st * 128);
-    stage_issue<32, 0>(rqh, stage + 0 * kPlaneBytes + 4096 * wv, col, q_rb, lane);
-    stage_issue<32, 0>(rql, stage + 1 * kPlaneBytes + 4096 * wv, col, q_rb, lane);
-    stage_issue<32, 0>(rkh, stage + 2 * kPlaneBytes + 4096 * wv, col, k_rb, lane);
-    stage_issue<32, 0>(rkl, stage + 3 * kPlaneBytes + 4096 * wv, col, k_rb, lane);
-  };
+  const uint32_t q_stride = (uint32_t)a.nq_cols * 2, k_stride = (uint32_t)a.nk_cols * 2;
+  const size_t qo = (size_t)layer * a.seq * a.nq_cols + (size_t)h * DH;
+  const size_t ko = (size_t)layer * a.seq * a.nk_cols + (size_t)kvh * DH;
+  const uint32_t q_len = (uint32_t)((((int64_t)(a.seq - 1) * a.nq_cols + DH) * 2 + 15) & ~int64_t(15));
+  const uint32_t k_len = (uint32_t)((((int64_t)(a.seq - 1) * a.nk_cols + DH) * 2 + 15) & ~int64_t(15));
+  const __amdgpu_buffer_rsrc_t rqh = make_rsrc(a.qh + qo, q_len), rql = make_rsrc(a.ql + qo, q_len);
+  const __amdgpu_buffer_rsrc_t rkh = make_rsrc(a.kh + ko, k_len), rkl = make_rsrc(a.kl + ko, k_len);
 
-  f32x4 acc[4][4];  // acc[i][j][e] = S[i0 + 16 i + s][j0 + 16 j + 4 q + e]
+  // the wave's query rows as B operands: query 32 wv + n, d_h 16 kb + 8 hl .. + 7
+  lstage<DH, kLQ>(rqh, rql, lds, q0, q_stride, wv, lane);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  u32x4 bqh[KB], bql[KB];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  issue(0);
-#pragma unroll
-  for (int st = 0; st < NSTEP; ++st) {
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's part of step st is in LDS
-    __syncthreads();                // every part
-    u32x4 ah[2][4], al[2][4], bh[2][4], bl[2][4];
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc) {
-      const bool kval = st * 64 + 32 * kc + 8 * q < DH;  // chunks past d_h belong to the next head
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        ah[kc][r] = stage_chunk(stage + 0 * kPlaneBytes, 64 * wm + 16 * r + s, 4 * kc + q);
-        al[kc][r] = stage_chunk(stage + 1 * kPlaneBytes, 64 * wm + 16 * r + s, 4 * kc + q);
-        bh[kc][r] = stage_chunk(stage + 2 * kPlaneBytes, 64 * wn + 16 * r + s, 4 * kc + q);
-        bl[kc][r] = stage_chunk(stage + 3 * kPlaneBytes, 64 * wn + 16 * r + s, 4 * kc + q);
-        if (!kval) ah[kc][r] = al[kc][r] = bh[kc][r] = bl[kc][r] = u32x4{0u, 0u, 0u, 0u};
-      }
-    }
-    if (st + 1 < NSTEP) {
-      __builtin_amdgcn_s_waitcnt(0);  // read out
-      __syncthreads();                // by every wave, before the next step overwrites
-      issue(st + 1);
-    }
-#pragma unroll
-    for (int kc = 0; kc < 2; ++kc)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          acc[i][j] = mfma(bh[kc][j], ah[kc][i], acc[i][j]);
-          acc[i][j] = mfma(bl[kc][j], ah[kc][i], acc[i][j]);
-          acc[i][j] = mfma(bh[kc][j], al[kc][i], acc[i][j]);
-        }
+  for (int kb = 0; kb < KB; ++kb) {
+    bqh[kb] = lchunk<DH>(lds, 32 * wv + n, 2 * kb + hl);
+    bql[kb] = lchunk<DH>(lds + kLQ * S::RB, 32 * wv + n, 2 * kb + hl);
   }
-  if (i0 >= a.seq || j0 >= a.seq) return;
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();  // the query tile is read out before key tile 0 overwrites it
+
+  const int n_kt = (a.seq + kLK - 1) / kLK;
+  lstage<DH, kLK>(rkh, rkl, lds, 0, k_stride, wv, lane);
 
   // S~ = (q . k) / (sqrt(d_h) scale), the factor formed in double
-  const float c = (float)(1.0 / (std::sqrt((double)DH) * (double)a.scale[layer]));
-  const bool words = (a.seq & 3) == 0;  // rows start 4-byte aligned
-  // A scaled logit that is not finite (a NaN or zero scale, an inf product)
-  // cannot be represented either: it counts as an overflow, and the maximum
-  // is kept on the bit patterns of |S~| (ordered as integers, +inf and NaN
-  // above every finite value), so a NaN or inf reaches max_abs.
-  int n_over = 0;
-  int mx = 0;
+  const float cf = (float)(1.0 / (std::sqrt((double)DH) * (double)a.scale[layer]));
+  const int query = q0 + 32 * wv + n;
+  const bool q_in = query < a.seq;
+  const bool rows_full = q0 + 32 * wv + 31 < a.seq;  // every query row of the wave exists
+  const int vec = (a.seq & 15) == 0 ? 2 : (a.seq & 3) == 0 ? 1 : 0;  // rows 16- / 4-byte aligned
+  uint8_t* const crow = a.codes ? a.codes + ((size_t)lh * a.seq + (q_in ? query : 0)) * a.seq : nullptr;
+  // A scaled logit that is not finite (a NaN or zero scale) cannot be
+  // represented either: it counts as an overflow, and the maximum is kept on
+  // the bit patterns of |S~| (ordered as integers, +inf and NaN above every
+  // finite value), so a NaN or inf reaches max_abs.  n_over counts lanes of
+  // whole-tile blocks through a wave-wide mask (the same for every lane), and
+  // per lane elsewhere.
+  int n_over_wave = 0, n_over = 0, mx = 0;
+  float mxf = 0.f;  // whole-tile blocks: max |S~|
+  // codes of the previous tile, stored during this one: after an exchange
+  // between lanes l and l + 32, lane l holds keys 32 mb + 16 hl .. + 15 of its
+  // query row in pend[mb] (words in key order)
+  u32x4 pend[kLMB];
+  int pend_key = -1;
+
+  auto store_codes = [&](int key_base) {
+    if (!crow || !q_in) return;
+    const bool full = key_base + kLK <= a.seq;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = i0 + 16 * i + s;
+    for (int mb = 0; mb < kLMB; ++mb) {
+      const int k0 = key_base + 32 * mb + 16 * hl;
+      if (full && vec == 2) {
+        *reinterpret_cast<u32x4*>(crow + k0) = pend[mb];
+      } else {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int col = j0 + 16 * j + 4 * q;
-      float v[4];
+        for (int q = 0; q < 4; ++q) {
+          const int key0 = k0 + 4 * q;
+          const uint32_t w = pend[mb][q];
+          if (vec >= 1 && key0 + 3 < a.seq) {
+            *reinterpret_cast<uint32_t*>(crow + key0) = w;
+          } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        v[e] = acc[i][j][e] * c;
-        const bool in = row < a.seq && col + e < a.seq;
-        const float av = fabsf(v[e]);
-        n_over += (in && !(av <= 448.f)) ? 1 : 0;
-        mx = in ? max(mx, __float_as_int(av)) : mx;
-      }
-      if (a.codes && row < a.seq) {
-        int w = __builtin_amdgcn_cvt_pk_fp8_f32(v[0], v[1], 0, false);
-        w = __builtin_amdgcn_cvt_pk_fp8_f32(v[2], v[3], w, true);
-        uint8_t* out = a.codes + (((size_t)layer * a.n_heads + h) * a.seq + row) * a.seq + col;
-        if (words && col + 3 < a.seq) {
-          *reinterpret_cast<int*>(out) = w;
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            if (col + e < a.seq) out[e] = (uint8_t)(w >> (8 * e));
+            for (int e = 0; e < 4; ++e)
+              if (key0 + e < a.seq) crow[key0 + e] = (uint8_t)(w >> (8 * e));
+          }
         }
       }
     }
+  };
+
+#pragma unroll 1
+  for (int kt = 0; kt < n_kt; ++kt) {
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's part of tile kt is in LDS
+    __syncthreads();                // every part, and tile kt - 1 fully read
+    if (kt + 1 < n_kt) lstage<DH, kLK>(rkh, rkl, lds + ((kt + 1) & 1) * S::TILE, (kt + 1) * kLK, k_stride, wv, lane);
+    if (pend_key >= 0) store_codes(pend_key);
+
+    const uint8_t* th = lds + (kt & 1) * S::TILE;
+    const uint8_t* tl = th + S::PLANE_K;
+    f32x16 acc[kLMB];
+#pragma unroll
+    for (int mb = 0; mb < kLMB; ++mb) acc[mb] = f32x16{};
+    // A operands of k block kb + 1 are read while the products of k block kb
+    // run; consecutive products go to independent accumulators
+    u32x4 kh[2][kLMB], kl[2][kLMB];
+#pragma unroll
+    for (int mb = 0; mb < kLMB; ++mb) {
+      kh[0][mb] = lchunk<DH>(th, 32 * mb + n, hl);
+      kl[0][mb] = lchunk<DH>(tl, 32 * mb + n, hl);
+    }
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const int cur = kb & 1;
+      if (kb + 1 < KB) {
+#pragma unroll
+        for (int mb = 0; mb < kLMB; ++mb) {
+          kh[cur ^ 1][mb] = lchunk<DH>(th, 32 * mb + n, 2 * (kb + 1) + hl);
+          kl[cur ^ 1][mb] = lchunk<DH>(tl, 32 * mb + n, 2 * (kb + 1) + hl);
+        }
+      }
+#pragma unroll
+      for (int mb = 0; mb < kLMB; ++mb) acc[mb] = mfma32(kh[cur][mb], bqh[kb], acc[mb]);
+#pragma unroll
+      for (int mb = 0; mb < kLMB; ++mb) acc[mb] = mfma32(kl[cur][mb], bqh[kb], acc[mb]);
+#pragma unroll
+      for (int mb = 0; mb < kLMB; ++mb) acc[mb] = mfma32(kh[cur][mb], bql[kb], acc[mb]);
+    }
+
+    // lane: query 32 wv + n; register r of block mb: key kt 64 + 32 mb + 8 (r / 4) + 4 hl + r % 4
+    const int key_base = kt * kLK;
+    auto epilogue = [&](auto whole_tag) {
+      constexpr bool WHOLE = decltype(whole_tag)::value;
+#pragma unroll
+      for (int mb = 0; mb < kLMB; ++mb) {
+        uint32_t w[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = acc[mb][4 * g + e] * cf;
+          if constexpr (WHOLE) {
+            // the NaN-propagating maximum keeps a NaN, as the bit patterns do below
+#pragma unroll
+            for (int e = 0; e < 4; ++e) n_over_wave += __popcll(__ballot(!(fabsf(v[e]) <= 448.f)));
+            mxf = __builtin_elementwise_maximum(
+                mxf, __builtin_elementwise_maximum(__builtin_elementwise_maximum(fabsf(v[0]), fabsf(v[1])),
+                                                   __builtin_elementwise_maximum(fabsf(v[2]), fabsf(v[3]))));
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int ab = __float_as_int(v[e]) & 0x7fffffff;  // bits of |S~|
+              const int key = key_base + 32 * mb + 8 * g + 4 * hl + e;
+              const bool in = q_in && key < a.seq;
+              n_over += (in && ab > 0x43E00000) ? 1 : 0;  // !(|S~| <= 448), NaN and inf included
+              mx = in ? max(mx, ab) : mx;
+            }
+          }
+          const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[0], v[1], 0, false);
+          w[g] = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(v[2], v[3], lo, true);
+        }
+        // keys 8 g + 4 hl .. + 3 in w[g]: lane l takes keys 0 .. 15 of the block, lane l + 32 keys 16 .. 31
+        const uint32_t y0 = (uint32_t)__shfl_xor((int)(hl ? w[0] : w[2]), 32);
+        const uint32_t y1 = (uint32_t)__shfl_xor((int)(hl ? w[1] : w[3]), 32);
+        pend[mb] = hl ? u32x4{y0, w[2], y1, w[3]} : u32x4{w[0], y0, w[1], y1};
+      }
+    };
+    if (rows_full && key_base + kLK <= a.seq)  // wave-uniform
+      epilogue(std::true_type{});
+    else
+      epilogue(std::false_type{});
+    pend_key = key_base;
   }
+  if (pend_key >= 0) store_codes(pend_key);
+  n_over += lane == 0 ? n_over_wave : 0;
+  mx = max(mx, __float_as_int(mxf) & 0x7fffffff);
+
   // per-head statistics: integer sum and integer maximum of the bit patterns
   // of non-negative floats are independent of the order of the atomics
 #pragma unroll
@@ -282,9 +405,8 @@ __global__ void __launch_bounds__(64 * kWaves) logits_kernel(LogitArgs a) {
     mx = max(mx, __shfl_xor(mx, m));
   }
   if (lane == 0) {
-    const int hl = layer * a.n_heads + h;
-    if (n_over) atomicAdd(a.n_over + hl, n_over);
-    atomicMax(reinterpret_cast<int32_t*>(a.max_abs) + hl, mx);
+    if (n_over) atomicAdd(a.n_over + lh, n_over);
+    atomicMax(reinterpret_cast<int32_t*>(a.max_abs) + lh, mx);
   }
 }
 
@@ -318,11 +440,12 @@ void sn_launch_proj(const ProjArgs& args, hipStream_t st) {
 }
 
 void sn_launch_logits(const LogitArgs& a, int head_dim, hipStream_t st) {
-  const dim3 grid(((a.layers * a.n_heads * a.tiles * a.tiles + 7) / 8) * 8);
+  const int n_qt = (a.seq + kLQ - 1) / kLQ;
+  const dim3 grid(((a.layers * a.n_heads * n_qt + 7) / 8) * 8);
   switch (head_dim) {
-    case 16: logits_kernel<16><<<grid, 64 * kWaves, 0, st>>>(a); break;
-    case 32: logits_kernel<32><<<grid, 64 * kWaves, 0, st>>>(a); break;
-    case 64: logits_kernel<64><<<grid, 64 * kWaves, 0, st>>>(a); break;
-    default: logits_kernel<128><<<grid, 64 * kWaves, 0, st>>>(a); break;
+    case 16: logits_kernel<16><<<grid, 64 * kLWaves, 0, st>>>(a); break;
+    case 32: logits_kernel<32><<<grid, 64 * kLWaves, 0, st>>>(a); break;
+    case 64: logits_kernel<64><<<grid, 64 * kLWaves, 0, st>>>(a); break;
+    default: logits_kernel<128><<<grid, 64 * kLWaves, 0, st>>>(a); break;
   }
 }

@@ -323,23 +323,28 @@ __global__ void __launch_bounds__(64 * kLWaves) __attribute__((amdgpu_waves_per_
     f32x16 acc[kLMB];
 #pragma unroll
     for (int mb = 0; mb < kLMB; ++mb) acc[mb] = f32x16{};
-    // A operands of k block kb + 1 are read while the products of k block kb
-    // run; consecutive products go to independent accumulators
-    u32x4 kh[2][kLMB], kl[2][kLMB];
+    // A operands of k block kb + 2 are read while the products of k block kb
+    // run (a ring of three operand sets; the scheduling barriers keep the
+    // compiler from folding the ring into one set, which would expose the
+    // LDS latency at every k block); consecutive products go to independent
+    // accumulators
+    constexpr int KR = 3;
+    u32x4 kh[KR][kLMB], kl[KR][kLMB];
+    auto read_kb = [&](int kb) {
 #pragma unroll
-    for (int mb = 0; mb < kLMB; ++mb) {
-      kh[0][mb] = lchunk<DH>(th, 32 * mb + n, hl);
-      kl[0][mb] = lchunk<DH>(tl, 32 * mb + n, hl);
-    }
+      for (int mb = 0; mb < kLMB; ++mb) {
+        kh[kb % KR][mb] = lchunk<DH>(th, 32 * mb + n, 2 * kb + hl);
+        kl[kb % KR][mb] = lchunk<DH>(tl, 32 * mb + n, 2 * kb + hl);
+      }
+    };
+#pragma unroll
+    for (int kb = 0; kb < KR - 1 && kb < KB; ++kb) read_kb(kb);
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      const int cur = kb & 1;
-      if (kb + 1 < KB) {
-#pragma unroll
-        for (int mb = 0; mb < kLMB; ++mb) {
-          kh[cur ^ 1][mb] = lchunk<DH>(th, 32 * mb + n, 2 * (kb + 1) + hl);
-          kl[cur ^ 1][mb] = lchunk<DH>(tl, 32 * mb + n, 2 * (kb + 1) + hl);
-        }
+      const int cur = kb % KR;
+      if (kb + KR - 1 < KB) {
+        read_kb(kb + KR - 1);
+        __builtin_amdgcn_sched_barrier(0);  // the reads of k block kb + 2 go first
       }
 #pragma unroll
       for (int mb = 0; mb < kLMB; ++mb) acc[mb] = mfma32(kh[cur][mb], bqh[kb], acc[mb]);
@@ -347,6 +352,7 @@ __global__ void __launch_bounds__(64 * kLWaves) __attribute__((amdgpu_waves_per_
       for (int mb = 0; mb < kLMB; ++mb) acc[mb] = mfma32(kl[cur][mb], bqh[kb], acc[mb]);
 #pragma unroll
       for (int mb = 0; mb < kLMB; ++mb) acc[mb] = mfma32(kh[cur][mb], bql[kb], acc[mb]);
+      __builtin_amdgcn_sched_barrier(0);  // then the products of k block kb
     }
 
     // lane: query 32 wv + n; register r of block mb: key kt 64 + 32 mb + 8 (r / 4) + 4 hl + r % 4

@@ -441,6 +441,7 @@ def bench_fp8(args):
     # one launch of each kernel covers every layer
     proj_flops = 2.0 * seq * wl.d_model * (wl.n_q + wl.n_kv) * wl.head_dim * wl.n_layers
     logit_flops = 3 * 2.0 * seq * seq * wl.head_dim * wl.n_q * wl.n_layers   # three bf16 products
+    logit_bytes = 4.0 * seq * (wl.n_q + wl.n_kv) * wl.head_dim * wl.n_layers + 1.0 * wl.n_layers * wl.n_q * seq * seq
     tflops = proj_flops / (p_ms / p_n * 1e-3) / 1e12
     logits = wl.n_layers * wl.n_q * seq * seq
     out = {
@@ -458,9 +459,20 @@ def bench_fp8(args):
         "roofline": {
             "kernel": "logits_projection (Q, K = X W^T, bf16 matrix cores)",
             "bound": "mfma", "achieved": tflops, "peak": 2500.0, "unit": "TFLOP/s", "frac": tflops / 2500.0,
-            "traffic": None, "algorithmic_flops_per_launch": proj_flops, "avg_launch_ms": p_ms / p_n,
-            "launches": p_n,
-            "logits_kernel_TFLOPs": logit_flops / (l_ms / max(l_n - 1, 1) * 1e-3) / 1e12,
+            "traffic": measured_traffic("proj"), "algorithmic_flops_per_launch": proj_flops,
+            "avg_launch_ms": p_ms / p_n, "launches": p_n,
+            "logits_kernel_TFLOPs": logit_flops / (l_ms / l_n * 1e-3) / 1e12,
+        },
+        # the logit kernel: three bf16 products per logit on the matrix cores, and its HBM
+        # stream (the Q, K hi/lo planes read once, one code byte written per logit)
+        "logits_roofline": {
+            "kernel": "logits_fp8 (S~ = Q K^T / (sqrt(d_h) scale) -> E4M3 codes, matrix cores)",
+            "bound": "mfma", "achieved": logit_flops / (l_ms / l_n * 1e-3) / 1e12, "peak": 2500.0,
+            "unit": "TFLOP/s", "frac": logit_flops / (l_ms / l_n * 1e-3) / 1e12 / 2500.0,
+            "traffic": measured_traffic("logits"), "algorithmic_flops_per_launch": logit_flops,
+            "algorithmic_bytes_per_launch": logit_bytes, "hbm_GBps": logit_bytes / (l_ms / l_n * 1e-3) / 1e9,
+            "hbm_frac": logit_bytes / (l_ms / l_n * 1e-3) / 1e9 / 8000.0, "avg_launch_ms": l_ms / l_n,
+            "launches": l_n,
         },
     }
     from paper_2602_18851_amd import fp8_report

@@ -343,8 +343,10 @@ def _run_full(wl, gq, gk, v0, n_iter, tol=0.0, flags=0):
 
 
 def _explicit_sample(wl, rng, every, edges):
-    """All heads of the first and last layer (with edges), then one seeded
-    head in every every-th layer."""
+    """Every head (every = 0); else all heads of the first and last layer
+    (with edges), then one seeded head in every every-th layer."""
+    if every == 0:
+        return [(l, h) for l in range(wl.n_layers) for h in range(wl.n_q)]
     heads = [(l, h) for l in (0, wl.n_layers - 1) for h in range(wl.n_q)] if edges else []
     for l in range(0, wl.n_layers, every):
         heads.append((l, int(rng.integers(wl.n_q))))
@@ -358,8 +360,10 @@ def test_full_size_every_head(key):
     chain; its own max over the layer's heads and Eq. "scale"), one layer at
     a time on the very weight bits and start vectors the GPU consumed; the
     iteration counts equal; every v within the informational cosine bar.
-    Then a seeded sample of heads against the explicit route (M = W^Q_h
-    W^{K T}_{g(h)} formed in float64, dense power iteration)."""
+    Then heads against the explicit route (M = W^Q_h W^{K T}_{g(h)} formed
+    in float64, dense power iteration): every head of GPT-2 XL, with each
+    layer's scale from its largest explicit sigma, and a seeded sample at the
+    7B and 70B shapes."""
     from oracle.explicit import dense_power_iteration, interaction_matrix
     wl = WORKLOADS[key]
     gq, gk = all_weights(wl, "cuda")
@@ -369,7 +373,7 @@ def test_full_size_every_head(key):
         assert np.isfinite(g["sigma"]).all() and (g["iters"] == wl.n_iter).all()
     v0c = v0.double().cpu().numpy()
     rng = np.random.default_rng(wl.cfg_id)
-    every, edges = {"gpt2-xl": (1, True), "llama2-7b-spiked": (4, False), "llama2-70b-gqa": (10, False)}[key]
+    every, edges = {"gpt2-xl": (0, True), "llama2-7b-spiked": (4, False), "llama2-70b-gqa": (10, False)}[key]
     sample = _explicit_sample(wl, rng, every, edges)
     worst = {form: [0.0, 0.0, 1.0] for form in FORMS}   # sigma err, scale err, min |cos v|
     e_worst = 0.0
@@ -386,19 +390,25 @@ def test_full_size_every_head(key):
             assert cos >= 1 - 1e-3, (form, l, cos)
             w = worst[form]
             w[0], w[1], w[2] = max(w[0], es), max(w[1], ec), min(w[2], cos)
-        for (ls, h) in sample:   # the explicit route on the seeded sample of this layer
+        sig_layer = []
+        for (ls, h) in sample:   # the explicit route on the heads of this layer in the sample
             if ls != l:
                 continue
             WQ, WK = head_slices(wq_l, wk_l, h, wl.n_kv, wl.head_dim)
             sig_e, _, _, it_e = dense_power_iteration(interaction_matrix(WQ, WK), v0c[l, h], wl.n_iter)
             assert it_e == wl.n_iter
+            sig_layer.append(sig_e)
             for form, g in gpu.items():
                 e = float(_rel(g["sigma"][l, h], sig_e))
                 assert e <= RTOL, (form, l, h, e)
                 e_worst = max(e_worst, e)
+        if len(sig_layer) == wl.n_q:   # every head of the layer: its scale from the explicit sigmas too
+            ref_scale = layer_scale(max(sig_layer), wl.alpha, wl.d_model, wl.head_dim)
+            for form, g in gpu.items():
+                assert _rel(g["scale"][l], ref_scale) <= RTOL, (form, l)
     print(f"{key}: all {wl.n_heads} heads and {wl.n_layers} scales, "
           + ", ".join(f"{f}: sigma {w[0]:.2e} scale {w[1]:.2e} min|cos v| {w[2]:.6f}" for f, w in worst.items())
-          + f"; explicit-M sample of {len(sample)} heads: {e_worst:.2e}")
+          + f"; explicit route on {len(sample)} heads: {e_worst:.2e}")
     del gq, gk
     torch.cuda.empty_cache()
 

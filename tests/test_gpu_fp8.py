@@ -45,9 +45,12 @@ def _pad(t, ld):
     return p.cuda()[..., :t.shape[-1]]
 
 
+def _f64(t):
+    return t if isinstance(t, np.ndarray) else t.double().numpy()
+
+
 def check_head(gpu_codes, gpu_max, gpu_over, x, wq, wk, scale, h, n_kv, dh):
-    x64 = x.double().numpy()
-    wq64, wk64 = wq.double().numpy(), wk.double().numpy()
+    x64, wq64, wk64 = _f64(x), _f64(wq), _f64(wk)
     S = fp8_consumer.head_logits(x64, wq64, wk64, h, n_kv, dh) / scale
     g = (wq64.shape[0] // dh) // n_kv
     qn = np.linalg.norm(x64 @ wq64[h * dh:(h + 1) * dh].T, axis=1)
@@ -178,7 +181,9 @@ def test_non_finite_scale_counts_every_logit_as_overflow():
 
 def test_full_size_70b_sampled_heads():
     """Llama-2-70B GQA shape, 1024 tokens per layer, all 80 layers on the GPU;
-    two heads of two layers against the oracle.  Per-layer scales are seeded
+    against the oracle, every code, max |S~| and overflow count of a seeded
+    sample of 147 heads: all 64 heads of the first and the last layer, and
+    one head in every fourth layer between.  Per-layer scales are seeded
     synthetic values around the size that puts the largest logit near 448."""
     wl = WORKLOADS["llama2-70b-gqa"]
     seq = 1024
@@ -189,10 +194,19 @@ def test_full_size_70b_sampled_heads():
     est = Spectral(wl.n_layers, wl.d_model, wl.n_q, wl.n_kv, wl.head_dim, wl.dtype, wl.alpha)
     max_abs, n_over, codes = est.logits_fp8(x, gq, gk, torch.from_numpy(scales).cuda(), want_codes=True)
     torch.cuda.synchronize()
-    for l, h in ((0, 0), (0, 37), (wl.n_layers - 1, 9), (wl.n_layers - 1, 63)):
-        check_head(codes[l, h].cpu().numpy(), max_abs[l, h].item(), n_over[l, h].item(), x[l].cpu(),
-                   gq[l].cpu(), gk[l].cpu(), float(scales[l]), h, wl.n_kv, wl.head_dim)
-    print(f"70B: max |S~| over all heads {max_abs.max().item():.1f}, overflowing heads "
+    sample = {0: range(wl.n_q), wl.n_layers - 1: range(wl.n_q)}
+    for l in range(4, wl.n_layers - 1, 4):
+        sample[l] = [int(rng.integers(wl.n_q))]
+    n_heads = 0
+    for l, heads in sorted(sample.items()):
+        x64, wq64, wk64 = x[l].cpu().double().numpy(), gq[l].cpu().double().numpy(), gk[l].cpu().double().numpy()
+        codes_l, max_l, over_l = codes[l].cpu().numpy(), max_abs[l].cpu().numpy(), n_over[l].cpu().numpy()
+        for h in heads:
+            check_head(codes_l[h], float(max_l[h]), int(over_l[h]), x64, wq64, wk64, float(scales[l]), h, wl.n_kv,
+                       wl.head_dim)
+            n_heads += 1
+    assert n_heads == 2 * wl.n_q + len(range(4, wl.n_layers - 1, 4))
+    print(f"70B: {n_heads} heads checked; max |S~| over all heads {max_abs.max().item():.1f}, overflowing heads "
           f"{int((n_over > 0).sum())} of {n_over.numel()}")
     est.close()
 

@@ -236,10 +236,11 @@ SN_API int spectral_step_layer(sn_ctx* ctx, const void* const* wq_layers, const 
  *   n_over     device int32 [n_layers][n_q]: #{(i, j): |S~_ij| > 448}.
  * A scaled logit that is not finite (a NaN or zero scale) counts as an
  * overflow and makes max_abs non-finite (NaN for a NaN scale).
- * Queued on the context's stream; allocates nothing; seq_len <= 46340.
- * The layer pointer table is written into the workspace by a kernel whose
- * launch arguments carry the pointers, so the call can be captured into a
- * HIP graph.
+ * Queued on the context's stream; allocates nothing; seq_len <= 46340, and
+ * one layer's W_Q (n_q * head_dim rows of ld bf16) below 4 GiB (else
+ * SN_EINVAL).  The layer pointer table is written into the workspace by a
+ * kernel whose launch arguments carry the pointers, so the call can be
+ * captured into a HIP graph.
  * Errors: SN_ENULL, SN_EINVAL, SN_EDTYPE, SN_ESTATE. */
 SN_API int spectral_logits_workspace_bytes(const sn_shape* shape, int32_t seq_len, int64_t* bytes);
 SN_API int spectral_logits_fp8(sn_ctx* ctx, const void* const* x_layers, int64_t ld_x, int32_t seq_len,

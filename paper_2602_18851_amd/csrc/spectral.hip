@@ -919,6 +919,9 @@ SN_API int spectral_logits_fp8(sn_ctx* c, const void* const* x_layers, int64_t l
   const int64_t nq_cols = (int64_t)sh.n_q_heads * dh, nk_cols = (int64_t)sh.n_kv_heads * dh;
   if ((int64_t)seq_len * ld_x * 2 >= (int64_t(1) << 31) || (int64_t)seq_len * nq_cols * 2 >= (int64_t(1) << 31))
     return fail(SN_EINVAL, "seq_len x row bytes must stay below 2^31");
+  // the projection reads a layer's weight rows through one buffer range
+  if (nq_cols * sh.ld * 2 >= (int64_t(1) << 32))
+    return fail(SN_EINVAL, "n_q_heads x head_dim x ld x 2 bytes (one layer's W_Q) must stay below 2^32");
   const int64_t tiles = ceil_div(seq_len, 128);
   if ((int64_t)L * sh.n_q_heads * tiles * tiles >= (int64_t(1) << 31) ||
       (int64_t)L * tiles * ceil_div(nq_cols + nk_cols, 128) >= (int64_t(1) << 31))

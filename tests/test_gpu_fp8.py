@@ -179,6 +179,27 @@ def test_non_finite_scale_counts_every_logit_as_overflow():
     est.close()
 
 
+def test_refuses_a_layer_weight_beyond_the_buffer_range():
+    """One layer's W_Q of 4 GiB or more (n_q d_h rows of ld bf16 elements)
+    does not fit the projection's buffer range: the call is refused with
+    SN_EINVAL before anything is queued (no weight is read, so the pointers
+    need not cover the shape)."""
+    from paper_2602_18851_amd.spectral import (SN_EINVAL, SpectralError, spectral_logits_fp8,
+                                               spectral_logits_workspace_bytes)
+    n_q, dh, ld, seq = 64, 128, 262144, 64   # 8192 rows x 512 KiB = 4 GiB
+    est = Spectral(1, 8192, n_q, 8, dh, "bf16", 0.02, ld=ld)
+    ws = torch.empty(spectral_logits_workspace_bytes(est.shape, seq), dtype=torch.uint8, device="cuda")
+    buf = torch.zeros(4096, dtype=torch.bfloat16, device="cuda")
+    max_abs = torch.zeros(n_q, device="cuda")
+    n_over = torch.zeros(n_q, dtype=torch.int32, device="cuda")
+    scale = torch.ones(1, device="cuda")
+    with pytest.raises(SpectralError) as err:
+        spectral_logits_fp8(est.ctx, [buf.data_ptr()], 0, seq, [buf.data_ptr()], [buf.data_ptr()], scale.data_ptr(),
+                            ws.data_ptr(), ws.numel(), 0, max_abs.data_ptr(), n_over.data_ptr())
+    assert err.value.code == SN_EINVAL and "2^32" in str(err.value)
+    est.close()
+
+
 def test_full_size_70b_sampled_heads():
     """Llama-2-70B GQA shape, 1024 tokens per layer, all 80 layers on the GPU;
     against the oracle, every code, max |S~| and overflow count of a seeded
